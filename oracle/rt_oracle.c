@@ -1,0 +1,370 @@
+/*
+ * Plain sequential CPU oracle: see rt_oracle.h for the contract.
+ *
+ * TEST INFRASTRUCTURE ONLY (tests, the smoke check and the CPU-baseline leg
+ * of the benchmark).  Written for clarity, not speed: one request at a time,
+ * every instance scored from scratch, one growable FIFO array per instance.
+ */
+#include "rt_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* The cost equation (Section III-A)                                         */
+/* ------------------------------------------------------------------------ */
+
+/* Ordering of costs for the argmin: smaller first, both zeros equal, NaN
+ * after +inf.  Costs are non-negative whenever the weights are, so the IEEE
+ * bit pattern of a positive float orders like its value. */
+static uint32_t cost_key(float c) {
+  uint32_t u;
+  if (c != c) return 0x7fc00000u;
+  if (c == 0.0f) return 0u;
+  memcpy(&u, &c, sizeof u);
+  return u;
+}
+
+/* cost = w_b * backlog * sigma  +  work * (1 + rho * press+) * sigma  +  w_q * queue
+ * with work = w_s * (request tokens) * tau, press+ = (occupancy + k) / cap.
+ * C evaluates each product and sum left to right in float32, which is the
+ * written order of the equation. */
+static float cost_eq(const orc_router* rp, float backlog_s, float work, float sg, int64_t kv_occ,
+                     int64_t k, float inv_cap, int64_t queue) {
+  float press = (float)(kv_occ + k) * inv_cap;
+  float load = rp->w_b * backlog_s * sg;
+  float size = work * (1.0f + rp->rho * press) * sg;
+  return load + size + rp->w_q * (float)queue;
+}
+
+/* Per-request priced work of a pool: prompt tokens at the prefill price
+ * ("scored analogously with p_r tau_pre"), predicted output tokens at the
+ * decode price. */
+static float pool_work(const orc_router* rp, int32_t pool, int32_t p, int32_t ohat) {
+  if (pool == ORC_PREFILL) return rp->w_s * (float)p * rp->tau_pre_s;
+  return rp->w_s * (float)ohat * rp->tau_dec_s;
+}
+
+/* Tokens the request adds to an instance's cache if admitted there. */
+static int64_t pool_need(int32_t pool, int32_t p, int32_t ohat) {
+  return pool == ORC_PREFILL ? (int64_t)p : (int64_t)p + (int64_t)ohat;
+}
+
+int orc_score(const orc_router* rp, int32_t pool, int32_t n_inst, const float* backlog_s,
+              const int32_t* queue, const int32_t* kv_occ, int64_t kv_cap, int64_t inst_stride,
+              int64_t n_req, const int32_t* prompt_len, const int32_t* pred_out_len,
+              const uint8_t* slo_class, int32_t* out_idx, float* out_score, float* out_second) {
+  if (!rp || n_inst < 1 || n_req < 0 || kv_cap < 1 || (pool != ORC_PREFILL && pool != ORC_DECODE))
+    return -1;
+  if (n_req > 0 && (!backlog_s || !queue || !kv_occ || !prompt_len || !pred_out_len || !slo_class ||
+                    !out_idx || !out_score))
+    return -1;
+  if (inst_stride != 0 && inst_stride < n_inst) return -1;
+  const float inv_cap = 1.0f / (float)kv_cap;
+  for (int64_t i = 0; i < n_req; ++i) {
+    const int32_t p = prompt_len[i], oh = pred_out_len[i];
+    const uint8_t c = slo_class[i];
+    if (p < 1 || (pool == ORC_DECODE && oh < 1) || c >= ORC_MAX_CLASSES) {
+      out_idx[i] = -1;
+      out_score[i] = NAN;
+      if (out_second) out_second[i] = NAN;
+      continue;
+    }
+    const float sg = rp->sigma[c];
+    const float work = pool_work(rp, pool, p, oh);
+    const int64_t k = pool_need(pool, p, oh);
+    const int64_t row = i * inst_stride;
+    int32_t best = -1;
+    float best_c = 0.0f, second_c = INFINITY;
+    for (int32_t j = 0; j < n_inst; ++j) {
+      float c_j = cost_eq(rp, backlog_s[row + j], work, sg, kv_occ[row + j], k, inv_cap, queue[row + j]);
+      if (best < 0 || cost_key(c_j) < cost_key(best_c)) {
+        if (best >= 0) second_c = best_c;
+        best = j;
+        best_c = c_j;
+      } else if (cost_key(c_j) < cost_key(second_c)) {
+        second_c = c_j;
+      }
+    }
+    out_idx[i] = best;
+    out_score[i] = best_c;
+    if (out_second) out_second[i] = second_c;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Replica simulation (Algorithm 1 per admission; Section III-D and          */
+/* Section VI serial-service model)                                          */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  int64_t busy;  /* time the instance finishes everything admitted so far */
+  int64_t queue; /* admitted and not yet finished                         */
+  int64_t kv;    /* cache tokens held by those requests                   */
+  int64_t pend;  /* tokens the router's ledger still prices for them      */
+  /* FIFO of in-flight requests in admission order: release time, cache
+   * tokens and priced tokens of each; entries [head, size) are in flight. */
+  int64_t *t_rel, *fp, *pt;
+  int64_t head, size, cap;
+} inst_t;
+
+static int push(inst_t* s, int64_t t_rel, int64_t fp, int64_t pt) {
+  if (s->size == s->cap) {
+    int64_t nc = s->cap ? 2 * s->cap : 16;
+    int64_t* a = (int64_t*)realloc(s->t_rel, (size_t)nc * sizeof(int64_t));
+    if (!a) return -1;
+    s->t_rel = a;
+    a = (int64_t*)realloc(s->fp, (size_t)nc * sizeof(int64_t));
+    if (!a) return -1;
+    s->fp = a;
+    a = (int64_t*)realloc(s->pt, (size_t)nc * sizeof(int64_t));
+    if (!a) return -1;
+    s->pt = a;
+    s->cap = nc;
+  }
+  s->t_rel[s->size] = t_rel;
+  s->fp[s->size] = fp;
+  s->pt[s->size] = pt;
+  s->size++;
+  s->queue += 1;
+  s->kv += fp;
+  s->pend += pt;
+  return 0;
+}
+
+/* Remove every request whose service has ended by `now` (a release at
+ * exactly `now` happens before the arrival at `now` is routed). */
+static int64_t retire(inst_t* s, int64_t now, int64_t* violations) {
+  int64_t popped = 0;
+  while (s->head < s->size && s->t_rel[s->head] <= now) {
+    s->queue -= 1;
+    s->kv -= s->fp[s->head];
+    s->pend -= s->pt[s->head];
+    s->head++;
+    popped++;
+    if (s->queue < 0 || s->kv < 0 || s->pend < 0) (*violations)++;
+  }
+  return popped;
+}
+
+static void free_pool(inst_t* a, int32_t n) {
+  if (!a) return;
+  for (int32_t j = 0; j < n; ++j) {
+    free(a[j].t_rel);
+    free(a[j].fp);
+    free(a[j].pt);
+  }
+  free(a);
+}
+
+/* backlog(d): seconds of work already committed to d.  True mode reads the
+ * simulation clock (busy-until minus now); proxy mode prices the in-flight
+ * ledger with the router's own constants (Section VI). */
+static float backlog_of(const orc_point* pt, int32_t pool, const inst_t* s, int64_t now) {
+  const orc_router* rp = &pt->router;
+  if (pt->backlog_mode == ORC_BACKLOG_TRUE) {
+    int64_t d = s->busy - now;
+    if (d < 0) d = 0;
+    return (float)d * 1e-9f;
+  }
+  if (pool == ORC_PREFILL) return rp->tau_pre_s * (float)s->pend + rp->pre_base_s * (float)s->queue;
+  return rp->tau_dec_s * (float)s->pend;
+}
+
+/* Own choice for one pool.  Returns the argmin; fills cost[] (learned only)
+ * and reports whether the best two costs are within tie_rel. */
+static int32_t choose(const orc_point* pt, int32_t pool, const inst_t* inst, int32_t n, int64_t r,
+                      int64_t now, int32_t p, int32_t ohat, uint8_t c, double tie_rel, float* cost,
+                      int* tie, int* close) {
+  *tie = 0;
+  *close = 0;
+  if (pt->policy == ORC_ROUND_ROBIN) return (int32_t)(r % n);
+  if (pt->policy == ORC_LEAST_LOADED) {
+    int32_t b = 0;
+    for (int32_t j = 1; j < n; ++j)
+      if (inst[j].queue < inst[b].queue) b = j;
+    return b;
+  }
+  const orc_router* rp = &pt->router;
+  const float sg = rp->sigma[c];
+  const float work = pool_work(rp, pool, p, ohat);
+  const int64_t k = pool_need(pool, p, ohat);
+  const int64_t cap = pool == ORC_PREFILL ? pt->kv_cap_pre : pt->kv_cap_dec;
+  const float inv_cap = 1.0f / (float)cap;
+  int32_t b = 0, b2 = -1;
+  for (int32_t j = 0; j < n; ++j) {
+    cost[j] = cost_eq(rp, backlog_of(pt, pool, &inst[j], now), work, sg, inst[j].kv, k, inv_cap,
+                      inst[j].queue);
+    if (j == 0) continue;
+    if (cost_key(cost[j]) < cost_key(cost[b])) {
+      b2 = b;
+      b = j;
+    } else if (b2 < 0 || cost_key(cost[j]) < cost_key(cost[b2])) {
+      b2 = j;
+    }
+  }
+  if (b2 >= 0) {
+    if (cost_key(cost[b2]) == cost_key(cost[b]))
+      *tie = 1;
+    else if ((double)cost[b2] - (double)cost[b] <= tie_rel * fabs((double)cost[b]))
+      *close = 1;
+  }
+  return b;
+}
+
+/* Adopt an external placement g in place of the own choice m. */
+static int32_t follow(const orc_point* pt, int32_t m, int32_t g, int32_t n, const float* cost,
+                      double tie_rel, int64_t* near_tie, int64_t* mismatch, int64_t* first, int64_t r) {
+  if (g == m) return m;
+  int ok = 0;
+  if (g >= 0 && g < n && pt->policy == ORC_LEARNED) {
+    double gap = (double)cost[g] - (double)cost[m];
+    ok = gap <= tie_rel * fabs((double)cost[m]);
+  }
+  if (ok) {
+    (*near_tie)++;
+  } else {
+    (*mismatch)++;
+    if (*first < 0) *first = r;
+  }
+  return (g >= 0 && g < n) ? g : m;
+}
+
+int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
+                    const int32_t* prompt_len, const int32_t* out_len,
+                    const int32_t* pred_out_len, const uint8_t* slo_class,
+                    const int32_t* follow_pre, const int32_t* follow_dec, double tie_rel,
+                    int32_t* i_pre, int32_t* i_dec, int64_t* ttft_ns, int64_t* span_ns,
+                    orc_stats* st) {
+  if (!pt || !st || n < 0) return -1;
+  if (pt->n_prefill < 1 || pt->n_decode < 1 || pt->n_classes < 1 ||
+      pt->n_classes > ORC_MAX_CLASSES || pt->kv_cap_pre < 1 || pt->kv_cap_dec < 1)
+    return -1;
+  if (n > 0 && (!arrival_ns || !prompt_len || !out_len || !pred_out_len || !slo_class || !i_pre ||
+                !i_dec || !ttft_ns || !span_ns))
+    return -1;
+  memset(st, 0, sizeof *st);
+  st->first_mismatch = -1;
+  const int32_t P = pt->n_prefill, D = pt->n_decode;
+  inst_t* pre = (inst_t*)calloc((size_t)P, sizeof(inst_t));
+  inst_t* dec = (inst_t*)calloc((size_t)D, sizeof(inst_t));
+  float* cost_pre = (float*)calloc((size_t)P, sizeof(float));
+  float* cost_dec = (float*)calloc((size_t)D, sizeof(float));
+  int rc = 0;
+  if (!pre || !dec || !cost_pre || !cost_dec) {
+    rc = -2;
+    goto done;
+  }
+
+  int64_t last_arrival = 0;
+  int have_arrival = 0;
+  for (int64_t r = 0; r < n; ++r) {
+    const int64_t now = arrival_ns[r];
+    const int32_t p = prompt_len[r], o = out_len[r], oh = pred_out_len[r];
+    const uint8_t c = slo_class[r];
+    /* Data checks: a rejected request is not routed and leaves no state. */
+    if (p < 1 || o < 1 || oh < 1 || c >= pt->n_classes || now < 0 ||
+        (have_arrival && now < last_arrival)) {
+      st->invalid++;
+      i_pre[r] = i_dec[r] = -1;
+      ttft_ns[r] = span_ns[r] = -1;
+      continue;
+    }
+    last_arrival = now;
+    have_arrival = 1;
+
+    /* 1. completions up to now leave both pools. */
+    for (int32_t j = 0; j < P; ++j) st->retired_pre += retire(&pre[j], now, &st->violations);
+    for (int32_t j = 0; j < D; ++j) st->retired_dec += retire(&dec[j], now, &st->violations);
+
+    /* 2. argmin of each pool, computed independently on the same state. */
+    int tie, close;
+    int32_t ip = choose(pt, ORC_PREFILL, pre, P, r, now, p, oh, c, tie_rel, cost_pre, &tie, &close);
+    st->tie_pre += tie;
+    st->close_pre += close;
+    int32_t id = choose(pt, ORC_DECODE, dec, D, r, now, p, oh, c, tie_rel, cost_dec, &tie, &close);
+    st->tie_dec += tie;
+    st->close_dec += close;
+    if (follow_pre)
+      ip = follow(pt, ip, follow_pre[r], P, cost_pre, tie_rel, &st->near_tie_pre, &st->mismatch_pre,
+                  &st->first_mismatch, r);
+    if (follow_dec)
+      id = follow(pt, id, follow_dec[r], D, cost_dec, tie_rel, &st->near_tie_dec, &st->mismatch_dec,
+                  &st->first_mismatch, r);
+
+    /* 3. prefill on ip, transfer the KV, decode on id: one request at a time
+     * per instance, in admission order. */
+    const int64_t s_pre = pt->pre_base_ns + (int64_t)p * pt->pre_tok_ns;
+    const int64_t s_dec = (int64_t)(o - 1) * pt->dec_tok_ns;
+    const int64_t xfer = (int64_t)p * pt->xfer_tok_ns;
+    inst_t* a = &pre[ip];
+    const int64_t pf_end = (now > a->busy ? now : a->busy) + s_pre;
+    if (a->size > a->head && pf_end < a->t_rel[a->size - 1]) st->violations++;
+    a->busy = pf_end;
+    if (push(a, pf_end, p, p)) {
+      rc = -2;
+      goto done;
+    }
+    if (a->kv > pt->kv_cap_pre) st->over_cap_pre++;
+    if (a->queue > st->max_queue_pre) st->max_queue_pre = a->queue;
+
+    inst_t* b = &dec[id];
+    const int64_t kv_at = pf_end + xfer;
+    const int64_t dec_end = (kv_at > b->busy ? kv_at : b->busy) + s_dec;
+    if (b->size > b->head && dec_end < b->t_rel[b->size - 1]) st->violations++;
+    b->busy = dec_end;
+    if (push(b, dec_end, (int64_t)p + o, oh)) {
+      rc = -2;
+      goto done;
+    }
+    if (b->kv > pt->kv_cap_dec) st->over_cap_dec++;
+    if (b->queue > st->max_queue_dec) st->max_queue_dec = b->queue;
+
+    /* 4. record the outcome. */
+    i_pre[r] = ip;
+    i_dec[r] = id;
+    ttft_ns[r] = pf_end - now;
+    span_ns[r] = dec_end - pf_end;
+  }
+
+  for (int32_t j = 0; j < P; ++j) st->end_inflight_pre += pre[j].queue;
+  for (int32_t j = 0; j < D; ++j) st->end_inflight_dec += dec[j].queue;
+  /* Drain: after every release everything must return to zero. */
+  for (int32_t j = 0; j < P; ++j) {
+    retire(&pre[j], INT64_MAX, &st->violations);
+    if (pre[j].queue || pre[j].kv || pre[j].pend) st->violations++;
+  }
+  for (int32_t j = 0; j < D; ++j) {
+    retire(&dec[j], INT64_MAX, &st->violations);
+    if (dec[j].queue || dec[j].kv || dec[j].pend) st->violations++;
+  }
+
+done:
+  free_pool(pre, P);
+  free_pool(dec, D);
+  free(cost_pre);
+  free(cost_dec);
+  return rc;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Goodput: SLO attainment under per-class TTFT/TPOT targets (Table II,      */
+/* Section IV-B).  TPOT = decode span / (o - 1); a one-token answer has no    */
+/* inter-token time and meets its TPOT target.                               */
+/* ------------------------------------------------------------------------ */
+int64_t orc_goodput(const orc_point* pt, int64_t n, const int32_t* out_len,
+                    const uint8_t* slo_class, const int64_t* ttft_ns, const int64_t* span_ns,
+                    double* goodput) {
+  int64_t met = 0;
+  for (int64_t r = 0; r < n; ++r) {
+    const uint8_t c = slo_class[r];
+    if (ttft_ns[r] < 0 || c >= ORC_MAX_CLASSES) continue;
+    const int ok_ttft = ttft_ns[r] <= pt->slo_ttft_ns[c];
+    const int ok_tpot = out_len[r] <= 1 || span_ns[r] <= pt->slo_tpot_ns[c] * (int64_t)(out_len[r] - 1);
+    if (ok_ttft && ok_tpot) met++;
+  }
+  if (goodput) *goodput = n > 0 ? (double)met / (double)n : 0.0;
+  return met;
+}
