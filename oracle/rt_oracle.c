@@ -65,7 +65,8 @@ int orc_score(const orc_router* rp, int32_t pool, int32_t n_inst, const float* b
   for (int64_t i = 0; i < n_req; ++i) {
     const int32_t p = prompt_len[i], oh = pred_out_len[i];
     const uint8_t c = slo_class[i];
-    if (p < 1 || (pool == ORC_DECODE && oh < 1) || c >= ORC_MAX_CLASSES) {
+    if (p < 1 || c >= ORC_MAX_CLASSES ||
+        (pool == ORC_DECODE && (oh < 1 || (int64_t)p + oh > INT32_MAX))) {
       out_idx[i] = -1;
       out_score[i] = NAN;
       if (out_second) out_second[i] = NAN;
@@ -265,8 +266,8 @@ int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
     const int32_t p = prompt_len[r], o = out_len[r], oh = pred_out_len[r];
     const uint8_t c = slo_class[r];
     /* Data checks: a rejected request is not routed and leaves no state. */
-    if (p < 1 || o < 1 || oh < 1 || c >= pt->n_classes || now < 0 ||
-        (have_arrival && now < last_arrival)) {
+    if (p < 1 || o < 1 || oh < 1 || (int64_t)p + o > INT32_MAX || (int64_t)p + oh > INT32_MAX ||
+        c >= pt->n_classes || now < 0 || (have_arrival && now < last_arrival)) {
       st->invalid++;
       i_pre[r] = i_dec[r] = -1;
       ttft_ns[r] = span_ns[r] = -1;

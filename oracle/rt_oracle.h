@@ -78,8 +78,9 @@ typedef struct {
  *   i*inst_stride (inst_stride 0 = one snapshot shared by all requests).
  *   out_idx[i] = argmin (lowest index on equal cost), out_score[i] = its cost;
  *   out_second[i] (may be NULL) = second-lowest cost (+inf if n_inst == 1).
- *   A request with prompt_len < 1, pred_out_len < 1 (decode pool) or
- *   slo_class >= ORC_MAX_CLASSES gets idx -1 and NaN scores.
+ *   A request with prompt_len < 1, slo_class >= ORC_MAX_CLASSES or (decode
+ *   pool) pred_out_len < 1 or prompt_len + pred_out_len >= 2^31 gets idx -1
+ *   and NaN scores.
  * Returns 0, or -1 on a bad argument. */
 int orc_score(const orc_router* rp, int32_t pool, int32_t n_inst, const float* backlog_s,
               const int32_t* queue, const int32_t* kv_occ, int64_t kv_cap, int64_t inst_stride,
@@ -91,7 +92,9 @@ int orc_score(const orc_router* rp, int32_t pool, int32_t n_inst, const float* b
  *   placements to adopt (see the header comment); tie_rel is the relative
  *   tolerance under which a divergent learned placement is accepted.
  *   Outputs: i_pre, i_dec, ttft_ns = prefill end - arrival,
- *   span_ns = decode end - prefill end; all -1 for a rejected request.
+ *   span_ns = decode end - prefill end; all -1 for a rejected request (a
+ *   length < 1, a token total p + o or p + o^ >= 2^31, a class out of range,
+ *   a negative arrival or one earlier than the previous accepted arrival).
  * Returns 0, -1 on a bad argument, -2 on allocation failure. */
 int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
                     const int32_t* prompt_len, const int32_t* out_len,

@@ -1,0 +1,236 @@
+// Standalone batched scorer (Section III-A cost equation + per-pool argmin)
+// and the per-replica goodput reduction (Section IV-B SLO targets, Table II
+// goodput), for gfx950.
+//
+// Shared snapshot (inst_stride 0): the instance terms that do not depend on
+// the request, w_b * backlog and w_q * queue, are formed once per block into
+// LDS (the same float32 operations the equation performs first), then each
+// thread scores kReq requests against every instance, reading each LDS entry
+// once for all of its requests.  VALU-bound.
+//
+// Per-request snapshot (inst_stride >= n_inst): a segment of S lanes per
+// request walks the request's row with unit stride across lanes (coalesced),
+// keeps a lane-local best, and reduces (key, index) over the segment.
+// HBM-bound.
+#include "rt_internal.h"
+
+namespace rt {
+namespace {
+
+constexpr int kReq = 4;       // requests per thread (shared snapshot)
+constexpr int kBlock = 256;
+
+struct SnapEntry {
+  float lb;    // w_b * backlog
+  float qq;    // w_q * (float)queue
+  int32_t kv;  // occupancy
+  int32_t pad;
+};
+
+__device__ __forceinline__ bool req_ok(int32_t pool, int32_t p, int32_t oh, uint32_t c) {
+  if (p < 1 || c >= (uint32_t)kMaxClasses) return false;
+  if (pool == 1 && (oh < 1 || (int64_t)p + oh > INT32_MAX)) return false;
+  return true;
+}
+
+// One thread's kReq requests against every snapshot entry.  kNonNeg: every
+// occupancy is >= 0, so occupancy + need < 2^32 and the sum converts exactly
+// through the unsigned 32-bit path (same value and rounding as int64).
+template <bool kNonNeg>
+__device__ __forceinline__ void score_loop(const SnapEntry* snap, int n, const ScoreArgs& a, const float* sg,
+                                           const float* work, const int64_t* need, uint32_t* bkey,
+                                           int32_t* bi) {
+  for (int j = 0; j < n; ++j) {
+    const SnapEntry e = snap[j];
+#pragma unroll
+    for (int r = 0; r < kReq; ++r) {
+      float press;
+      if constexpr (kNonNeg)
+        press = (float)((uint32_t)e.kv + (uint32_t)need[r]) * a.inv_cap;
+      else
+        press = (float)((int64_t)e.kv + need[r]) * a.inv_cap;
+      const float load = e.lb * sg[r];
+      const float size = work[r] * (1.0f + a.rho * press) * sg[r];
+      const float cost = load + size + e.qq;
+      const uint32_t k = cost_key(cost);
+      if (k < bkey[r]) {
+        bkey[r] = k;
+        bi[r] = j;
+      }
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) score_shared_kernel(ScoreArgs a) {
+  extern __shared__ SnapEntry snap[];
+  const int n = a.n_inst;
+  int nonneg = 1;
+  for (int j = threadIdx.x; j < n; j += kBlock) {
+    SnapEntry e;
+    e.lb = a.w_b * a.backlog[j];
+    e.qq = a.w_q * (float)a.queue[j];
+    e.kv = a.kv[j];
+    e.pad = 0;
+    nonneg &= e.kv >= 0;
+    snap[j] = e;
+  }
+  nonneg = __syncthreads_and(nonneg);
+
+  const int64_t first = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kReq;
+  float sg[kReq], work[kReq];
+  int64_t need[kReq];
+  int32_t bi[kReq];
+  uint32_t bkey[kReq];
+  bool ok[kReq];
+#pragma unroll
+  for (int r = 0; r < kReq; ++r) {
+    const int64_t i = first + r;
+    ok[r] = false;
+    sg[r] = 0.0f;
+    work[r] = 0.0f;
+    need[r] = 0;
+    bi[r] = -1;
+    bkey[r] = 0xffffffffu;
+    if (i < a.n_req) {
+      const int32_t p = a.plen[i];
+      const int32_t oh = a.pool == 1 ? a.ohat[i] : 0;
+      const uint32_t c = a.cls[i];
+      ok[r] = req_ok(a.pool, p, oh, c);
+      if (ok[r]) {
+        sg[r] = a.sigma[c];
+        work[r] = a.pool == 1 ? a.w_s * (float)oh * a.tau : a.w_s * (float)p * a.tau;
+        need[r] = a.pool == 1 ? (int64_t)p + oh : (int64_t)p;
+      }
+    }
+  }
+  if (nonneg)
+    score_loop<true>(snap, n, a, sg, work, need, bkey, bi);
+  else
+    score_loop<false>(snap, n, a, sg, work, need, bkey, bi);
+#pragma unroll
+  for (int r = 0; r < kReq; ++r) {
+    const int64_t i = first + r;
+    if (i < a.n_req) {
+      a.out_idx[i] = ok[r] ? bi[r] : -1;
+      a.out_score[i] = __uint_as_float(ok[r] ? bkey[r] : 0x7fc00000u);
+    }
+  }
+}
+
+template <int S>
+__global__ void __launch_bounds__(kBlock) score_rows_kernel(ScoreArgs a) {
+  constexpr int kSegs = 64 / S;
+  const int lane = threadIdx.x & 63;
+  const int sl = lane % S;
+  const int64_t i = ((int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6)) * kSegs + lane / S;
+  const bool live = i < a.n_req;
+  int32_t p = 0, oh = 0;
+  uint32_t c = 0;
+  if (live) {
+    p = a.plen[i];
+    oh = a.pool == 1 ? a.ohat[i] : 0;
+    c = a.cls[i];
+  }
+  const bool ok = live && req_ok(a.pool, p, oh, c);
+  uint64_t best = ~0ull;  // (key << 32) | index
+  if (ok) {
+    const float sg = a.sigma[c];
+    const float work = a.pool == 1 ? a.w_s * (float)oh * a.tau : a.w_s * (float)p * a.tau;
+    const int64_t need = a.pool == 1 ? (int64_t)p + oh : (int64_t)p;
+    const int64_t row = i * a.stride;
+    for (int j = sl; j < a.n_inst; j += S) {
+      const float press = (float)((int64_t)a.kv[row + j] + need) * a.inv_cap;
+      const float load = a.w_b * a.backlog[row + j] * sg;
+      const float size = work * (1.0f + a.rho * press) * sg;
+      const float cost = load + size + a.w_q * (float)a.queue[row + j];
+      const uint64_t k = ((uint64_t)cost_key(cost) << 32) | (uint32_t)j;
+      best = k < best ? k : best;
+    }
+  }
+#pragma unroll
+  for (int m = 1; m < S; m <<= 1) {
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)best, m, 64);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(best >> 32), m, 64);
+    const uint64_t o = ((uint64_t)hi << 32) | lo;
+    best = o < best ? o : best;
+  }
+  if (live && sl == 0) {
+    a.out_idx[i] = ok ? (int32_t)(uint32_t)best : -1;
+    a.out_score[i] = __uint_as_float(ok ? (uint32_t)(best >> 32) : 0x7fc00000u);
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) goodput_kernel(GoodputArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t rep = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  if (rep >= a.n_replicas) return;  // whole wave leaves together
+  const int64_t lo = a.offsets[rep], hi = a.offsets[rep + 1];
+  const int pid = a.param_point ? a.param_point[rep] : 0;
+  if (lo < 0 || hi < lo || hi > a.n_requests || pid < 0 || pid >= a.n_points) {
+    // a replica this trace does not describe consistently: no read outside it
+    if (lane == 0) {
+      a.goodput[rep] = 0.0;
+      if (a.met) a.met[rep] = -1;
+      atomicOr(a.flag, kFlagBadTrace);
+    }
+    return;
+  }
+  const DevPoint& pp = a.points[pid];
+  int64_t met = 0;
+  for (int64_t i = lo + lane; i < hi; i += 64) {
+    const int64_t tt = a.ttft[i], sp = a.span[i];
+    const int32_t o = a.olen[i];
+    const uint32_t c = a.cls[i];
+    if (tt < 0 || c >= (uint32_t)kMaxClasses) continue;
+    const bool ok_ttft = tt <= pp.slo_ttft[c];
+    const bool ok_tpot = o <= 1 || sp <= pp.slo_tpot[c] * (int64_t)(o - 1);
+    met += (ok_ttft && ok_tpot) ? 1 : 0;
+  }
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) {
+    const uint32_t l = (uint32_t)__shfl_xor((int)(uint32_t)met, m, 64);
+    const uint32_t h = (uint32_t)__shfl_xor((int)(uint32_t)((uint64_t)met >> 32), m, 64);
+    met += (int64_t)(((uint64_t)h << 32) | l);
+  }
+  if (lane == 0) {
+    const int64_t n = hi - lo;
+    a.goodput[rep] = n > 0 ? (double)met / (double)n : 0.0;
+    if (a.met) a.met[rep] = met;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_score(const ScoreArgs& a, hipStream_t stream) {
+  if (a.n_req <= 0) return hipSuccess;
+  if (a.stride == 0) {
+    const int64_t per_block = (int64_t)kBlock * kReq;
+    const int64_t blocks = (a.n_req + per_block - 1) / per_block;
+    const size_t lds = sizeof(SnapEntry) * (size_t)a.n_inst;
+    hipLaunchKernelGGL(score_shared_kernel, dim3((unsigned)blocks), dim3(kBlock), lds, stream, a);
+    return hipGetLastError();
+  }
+  int S = 1;
+  while (S < a.n_inst && S < 64) S <<= 1;
+  const int64_t per_block = (kBlock / 64) * (64 / S);
+  const unsigned blocks = (unsigned)((a.n_req + per_block - 1) / per_block);
+  switch (S) {
+    case 1: hipLaunchKernelGGL(score_rows_kernel<1>, dim3(blocks), dim3(kBlock), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL(score_rows_kernel<2>, dim3(blocks), dim3(kBlock), 0, stream, a); break;
+    case 4: hipLaunchKernelGGL(score_rows_kernel<4>, dim3(blocks), dim3(kBlock), 0, stream, a); break;
+    case 8: hipLaunchKernelGGL(score_rows_kernel<8>, dim3(blocks), dim3(kBlock), 0, stream, a); break;
+    case 16: hipLaunchKernelGGL(score_rows_kernel<16>, dim3(blocks), dim3(kBlock), 0, stream, a); break;
+    case 32: hipLaunchKernelGGL(score_rows_kernel<32>, dim3(blocks), dim3(kBlock), 0, stream, a); break;
+    default: hipLaunchKernelGGL(score_rows_kernel<64>, dim3(blocks), dim3(kBlock), 0, stream, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_goodput(const GoodputArgs& a, hipStream_t stream) {
+  if (a.n_replicas <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((a.n_replicas + 3) / 4);
+  hipLaunchKernelGGL(goodput_kernel, dim3(blocks), dim3(kBlock), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace rt

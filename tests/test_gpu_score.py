@@ -1,0 +1,93 @@
+"""Standalone scorer on the GPU vs the oracle (Section III-A cost equation,
+per-pool argmin): the full-size 1,048,576 x 64 shared snapshot, per-request
+snapshots with ragged pool widths, both pools, rejected requests."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2609_16206_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+TIE_REL = 1e-6
+
+
+def _gpu_score(params, pool, d, n_req, n_inst, stride, kv_cap):
+    from paper_2609_16206_amd import rt_router as R
+    dev = "cuda"
+    t = {k: torch.from_numpy(np.ascontiguousarray(d[k])).to(dev)
+         for k in ("backlog_s", "queue", "kv_occ", "prompt_len", "pred_out_len", "slo_class")}
+    idx = torch.empty(n_req, dtype=torch.int32, device=dev)
+    sc = torch.empty(n_req, dtype=torch.float32, device=dev)
+    R.rt_score_argmin(params, pool, n_inst, t["backlog_s"], t["queue"], t["kv_occ"], kv_cap, stride, n_req,
+                      t["prompt_len"], t["pred_out_len"], t["slo_class"], idx, sc)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), sc.cpu().numpy()
+
+
+def _compare(params, pool, d, n_inst, stride, kv_cap):
+    n_req = d["prompt_len"].size
+    gi, gs = _gpu_score(params, pool, d, n_req, n_inst, stride, kv_cap)
+    oi, os_, osec = O.score(params, pool, d["backlog_s"], d["queue"], d["kv_occ"], kv_cap, n_inst, stride,
+                            d["prompt_len"], d["pred_out_len"], d["slo_class"])
+    bad = oi < 0
+    assert np.array_equal(gi[bad], oi[bad]) and np.isnan(gs[bad]).all()
+    diff = (gi != oi) & ~bad
+    # a different index is accepted only as a near tie of the oracle's best two
+    near = diff & ((osec - os_) <= TIE_REL * np.abs(os_))
+    assert np.array_equal(diff, near), f"{int((diff & ~near).sum())} placements beyond tolerance"
+    same = ~diff & ~bad
+    assert np.array_equal(gs[same].view(np.uint32), os_[same].view(np.uint32)), "scores differ bitwise"
+    return int(diff.sum())
+
+
+def test_scorer_full_size_shared_snapshot():
+    d = W.scorer_inputs(n_req=1 << 20, n_inst=64, seed=1)
+    prm = W.scorer_params()
+    ties = _compare(prm, "decode", d, 64, 0, d["kv_cap"])
+    print(f"scorer 1048576x64 shared: near-tie divergences {ties}", flush=True)
+
+
+@pytest.mark.parametrize("n_inst", [1, 3, 17, 64, 65, 200, 1024])
+def test_scorer_shared_ragged_widths(n_inst):
+    d = W.scorer_inputs(n_req=4099, n_inst=n_inst, seed=10 + n_inst)
+    prm = W.scorer_params()
+    _compare(prm, "decode", d, n_inst, 0, d["kv_cap"])
+    _compare(prm, "prefill", d, n_inst, 0, d["kv_cap"])
+
+
+@pytest.mark.parametrize("n_inst,stride", [(1, 1), (3, 3), (8, 11), (64, 64), (65, 65), (300, 301), (1024, 1024)])
+def test_scorer_per_request_snapshots(n_inst, stride):
+    n_req = 20_001 if n_inst <= 64 else 2_001
+    d = W.scorer_inputs(n_req=n_req, n_inst=stride, seed=100 + n_inst, per_request=True)
+    prm = W.scorer_params()
+    _compare(prm, "decode", d, n_inst, stride, d["kv_cap"])
+    _compare(prm, "prefill", d, n_inst, stride, d["kv_cap"])
+
+
+def test_scorer_rejected_requests_and_negative_occupancy():
+    d = W.scorer_inputs(n_req=1000, n_inst=40, seed=5)
+    d["prompt_len"][::7] = 0
+    d["pred_out_len"][3::11] = 0
+    d["slo_class"][5::13] = 9
+    d["prompt_len"][6] = 2 ** 30
+    d["pred_out_len"][6] = 2 ** 30
+    d["kv_occ"][4] = -5000  # takes the general (int64) conversion path
+    prm = W.scorer_params()
+    _compare(prm, "decode", d, 40, 0, d["kv_cap"])
+    _compare(prm, "prefill", d, 40, 0, d["kv_cap"])
+
+
+def test_scorer_hand_examples():
+    import json, os
+    cases = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "score_hand_examples.json")))["cases"]
+    for c in cases:
+        n = len(c["costs"])
+        d = dict(backlog_s=np.array(c["instances"]["backlog_s"], np.float32),
+                 queue=np.array(c["instances"]["queue"], np.int32),
+                 kv_occ=np.array(c["instances"]["kv_occ"], np.int32),
+                 prompt_len=np.array([c["request"]["prompt_len"]], np.int32),
+                 pred_out_len=np.array([c["request"]["pred_out_len"]], np.int32),
+                 slo_class=np.array([c["request"]["slo_class"]], np.uint8))
+        gi, gs = _gpu_score(c["router"], c["pool"], d, 1, n, 0, c["kv_cap"])
+        assert gi[0] == c["argmin"] and float(gs[0]) == min(c["costs"])

@@ -1,0 +1,136 @@
+"""Replica simulation on the GPU vs the oracle (Algorithm 1 on the
+serial-service simulator): the tiny 3P+3D workload in full under every policy
+and backlog mode, the paper-shaped 2P+6D cluster (4,096 x 10,000) in full, and
+edge cases: ragged and empty replicas, rejected requests, simultaneous
+arrivals, mixed pool shapes in one batch (every kernel class), determinism and
+replica-range resume."""
+import numpy as np
+import pytest
+
+from paper_2609_16206_amd import workload as W
+from tests.gpu_common import log, run_sim
+from tests.parity import check_properties, follow_replicas, goodput_recount
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("policy,mode", [("learned", "true"), ("learned", "proxy"), ("round_robin", "true"),
+                                         ("least_loaded", "true")])
+def test_tiny_full(policy, mode):
+    wl = W.tiny_sim()
+    pts = [dict(wl.points[0], policy=policy, backlog_mode=mode)]
+    tr = W.make_trace(wl)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    rep = follow_replicas(pts, tr, gpu, [0], gpu_goodput=g, gpu_met=met)
+    log(f"tiny {policy}/{mode}: {rep}, goodput {g[0]:.4f}")
+    if policy == "round_robin":
+        r = np.arange(2000)
+        assert np.array_equal(gpu["i_pre"], r % 3) and np.array_equal(gpu["i_dec"], r % 3)
+
+
+def test_cluster_full_size():
+    wl = W.paper_cluster()
+    tr = W.make_trace(wl)
+    log(f"cluster trace: {tr['arrival_ns'].size} requests")
+    gpu, g, met, flags = run_sim(wl.points, tr)
+    assert flags == 0
+    check_properties(wl.points, tr, gpu)
+    assert np.array_equal(goodput_recount(wl.points, tr, gpu), met)
+    rep = follow_replicas(wl.points, tr, gpu, range(wl.n_replicas), gpu_goodput=g, gpu_met=met)
+    log(f"cluster 4096x10000: {rep}; mean goodput {g.mean():.4f}")
+
+
+def _mixed_points():
+    """Pool shapes that exercise every kernel class, with all policies/modes."""
+    shapes = [(1, 1), (2, 2), (3, 4), (2, 6), (5, 16), (2, 32), (33, 64), (70, 100), (128, 1024), (1000, 300)]
+    pts = []
+    for k, (P, D) in enumerate(shapes):
+        pol = ("learned", "learned", "round_robin", "least_loaded")[k % 4]
+        mode = ("true", "proxy")[(k // 2) % 2]
+        pts.append(W.make_point(P, D, n_classes=3, policy=pol, backlog_mode=mode, kv_cap=50_000))
+    return pts
+
+
+def _ragged_trace(pts, lengths, seed=7, rate_scale=1.0):
+    parts, pp = [], []
+    tr0 = W.mixed_bursty()
+    for i, n in enumerate(lengths):
+        pid = i % len(pts)
+        traf = tr0.scaled(rate_scale * W.capacity_rps(pts[pid], tr0) / tr0.mean_rate())
+        parts.append(W.replica_arrays(seed, i, traf, n))
+        pp.append(pid)
+    keys = ("arrival_ns", "prompt_len", "out_len", "pred_out_len", "slo_class")
+    tr = {k: np.concatenate([q[k] for q in parts]) for k in keys}
+    tr["offsets"] = np.concatenate(([0], np.cumsum(lengths))).astype(np.int64)
+    tr["param_point"] = np.array(pp, np.int32)
+    return tr
+
+
+def test_mixed_shapes_ragged_lengths():
+    pts = _mixed_points()
+    lengths = [0, 1, 2, 63, 64, 65, 500, 3000, 1, 0, 777, 4096, 129, 2, 3, 5000, 40, 41, 0, 1200] * 3
+    tr = _ragged_trace(pts, lengths)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    check_properties(pts, tr, gpu)
+    assert np.array_equal(goodput_recount(pts, tr, gpu), met)
+    rep = follow_replicas(pts, tr, gpu, range(len(lengths)), gpu_goodput=g, gpu_met=met)
+    log(f"mixed shapes: {rep}")
+    assert np.all(g[np.array(lengths) == 0] == 0.0)
+
+
+def test_overload_deep_queues():
+    """Arrivals at 3x capacity: long FIFOs, many pops per step."""
+    pts = [W.make_point(2, 3, n_classes=3), W.make_point(2, 6, n_classes=3, backlog_mode="proxy"),
+           W.make_point(3, 40, n_classes=3, policy="least_loaded")]
+    tr = _ragged_trace(pts, [4000] * 12, seed=11, rate_scale=3.0)
+    gpu, g, met, flags = run_sim(pts, tr)
+    rep = follow_replicas(pts, tr, gpu, range(12), gpu_goodput=g, gpu_met=met)
+    log(f"overload: {rep}")
+
+
+def test_simultaneous_arrivals_and_rejections():
+    pts = [W.make_point(3, 5, n_classes=2), W.make_point(2, 2, n_classes=2, policy="round_robin")]
+    rng = np.random.default_rng(3)
+    n = 3000
+    lengths = [n, n, n, n]
+    tr = _ragged_trace(pts, lengths, seed=21)
+    # coarse arrival grid: many equal timestamps
+    tr["arrival_ns"] = (tr["arrival_ns"] // 500_000_000) * 500_000_000
+    for i in range(4):
+        s = slice(i * n, (i + 1) * n)
+        tr["arrival_ns"][s] = np.sort(tr["arrival_ns"][s])
+    bad = rng.choice(4 * n, 60, replace=False)
+    kinds = np.arange(60) % 6
+    tr["prompt_len"][bad[kinds == 0]] = 0
+    tr["out_len"][bad[kinds == 1]] = 0
+    tr["pred_out_len"][bad[kinds == 2]] = -3
+    tr["slo_class"][bad[kinds == 3]] = 2
+    tr["arrival_ns"][bad[kinds == 4]] = -1
+    b5 = bad[kinds == 5]
+    tr["prompt_len"][b5] = 2 ** 30
+    tr["out_len"][b5] = 2 ** 30
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 1
+    assert (gpu["ttft_ns"] < 0).sum() >= 50
+    rep = follow_replicas(pts, tr, gpu, range(4), gpu_goodput=g, gpu_met=met)
+    log(f"ties+rejections: {rep}")
+    assert rep["invalid"] == int((gpu["ttft_ns"] < 0).sum())
+
+
+def test_determinism_and_range_resume():
+    wl = W.paper_cluster(n_replicas=300, requests=3000)
+    tr = W.make_trace(wl)
+    a, ga, _, _ = run_sim(wl.points, tr)
+    b, gb, _, _ = run_sim(wl.points, tr)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+    assert np.array_equal(ga, gb)
+    # replicas [117, 211) alone, as their own batch
+    sub = W.make_trace(wl, replicas=range(117, 211))
+    c, gc, _, _ = run_sim(wl.points, sub)
+    s = slice(117 * 3000, 211 * 3000)
+    for k in a:
+        assert np.array_equal(a[k][s], c[k]), k
+    assert np.array_equal(ga[117:211], gc)

@@ -181,12 +181,12 @@ def test_per_request_snapshot_rows():
 
 def test_invalid_requests_flagged():
     snap = dict(backlog_s=np.zeros(3, np.float32), queue=np.zeros(3, np.int32), kv_occ=np.zeros(3, np.int32))
-    p = np.array([0, 5, 5, 5], np.int32)
-    oh = np.array([5, 0, 5, 5], np.int32)
-    c = np.array([0, 0, 8, 7], np.uint8)
+    p = np.array([0, 5, 5, 5, 2 ** 30], np.int32)
+    oh = np.array([5, 0, 5, 5, 2 ** 30], np.int32)
+    c = np.array([0, 0, 8, 7, 0], np.uint8)
     idx, sc, _ = O.score(BASE, "decode", snap["backlog_s"], snap["queue"], snap["kv_occ"], 1000, 3, 0, p, oh, c)
-    assert list(idx) == [-1, -1, -1, 0]
-    assert np.isnan(sc[:3]).all() and np.isfinite(sc[3])
+    assert list(idx) == [-1, -1, -1, 0, -1]
+    assert np.isnan(sc[[0, 1, 2, 4]]).all() and np.isfinite(sc[3])
     # prefill does not read the predicted length
     idx, _, _ = O.score(BASE, "prefill", snap["backlog_s"], snap["queue"], snap["kv_occ"], 1000, 3, 0, p, oh, c)
-    assert list(idx) == [-1, 0, -1, 0]
+    assert list(idx) == [-1, 0, -1, 0, 0]

@@ -282,7 +282,7 @@ def test_invalid_requests_are_skipped_without_side_effects():
     arr, p, o, oh, c = _trace(400, rng, n_classes=2)
     pt = W.make_point(2, 3, n_classes=2)
     good, _ = O.sim_replica(pt, arr, p, o, oh, c)
-    bad_after = {3: "p0", 50: "o0", 51: "oh0", 200: "class", 399: "early"}
+    bad_after = {3: "p0", 50: "o0", 51: "oh0", 120: "big", 200: "class", 399: "early"}
     A, Pp, Oo, OH, CC = [], [], [], [], []
     for r in range(400):
         A.append(arr[r]); Pp.append(p[r]); Oo.append(o[r]); OH.append(oh[r]); CC.append(c[r])
@@ -295,12 +295,13 @@ def test_invalid_requests_are_skipped_without_side_effects():
         if kind == "oh0": ohh = 0
         if kind == "class": cc = 2
         if kind == "early": a = arr[r] - 1
+        if kind == "big": pp, oo = 2 ** 30, 2 ** 30  # token total 2^31 does not fit int32
         A.append(a); Pp.append(pp); Oo.append(oo); OH.append(ohh); CC.append(cc)
     out, st = O.sim_replica(pt, np.array(A, np.int64), np.array(Pp, np.int32), np.array(Oo, np.int32),
                             np.array(OH, np.int32), np.array(CC, np.uint8))
-    assert st["invalid"] == 5
+    assert st["invalid"] == 6
     bad = out["ttft_ns"] < 0
-    assert bad.sum() == 5
+    assert bad.sum() == 6
     for k in out:
         assert np.all(out[k][bad] == -1)
         assert np.array_equal(out[k][~bad], good[k])
