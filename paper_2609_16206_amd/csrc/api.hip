@@ -128,6 +128,10 @@ struct rt_sim {
   hipEvent_t t0 = nullptr, t1 = nullptr;
   double timed_ms = 0.0;
   int64_t timed_calls = 0;
+  // internal streams (default priority) that run kernel classes side by side
+  std::vector<hipStream_t> lanes;
+  std::vector<hipEvent_t> joins;
+  hipEvent_t fork = nullptr;
 };
 
 static rt_status collect_timing(rt_sim* sim) {
@@ -209,6 +213,9 @@ rt_status rt_sim_destroy(rt_sim* sim) {
   if (sim->upload_done) (void)hipEventDestroy(sim->upload_done);
   if (sim->t0) (void)hipEventDestroy(sim->t0);
   if (sim->t1) (void)hipEventDestroy(sim->t1);
+  for (hipStream_t l : sim->lanes) (void)hipStreamDestroy(l);
+  for (hipEvent_t j : sim->joins) (void)hipEventDestroy(j);
+  if (sim->fork) (void)hipEventDestroy(sim->fork);
   delete sim;
   return RT_OK;
 }
@@ -273,9 +280,10 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
     });
 
   hipError_t e;
-  // Scratch: successor records, 40 bytes per request.
+  // Scratch: successor records (40 bytes per request) and the dummy slots.
   const size_t nreq = (size_t)trace->n_requests;
-  const size_t need = nreq * 40 + 256;
+  const size_t dummy_bytes = (size_t)rt::kDummyLanes * 64;
+  const size_t need = nreq * 40 + dummy_bytes + 256;
   if (need > sim->scratch_bytes) {
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
     if (sim->d_scratch) (void)hipFree(sim->d_scratch);
@@ -333,20 +341,52 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   a.i_dec = out->i_dec;
   a.ttft = out->ttft_ns;
   a.span = out->decode_span_ns;
-  a.sp_t = (int64_t*)sc;
-  a.sp_m = (int2*)(sc + nreq * 8);
-  a.sd_t = (int64_t*)(sc + nreq * 16);
-  a.sd_m = (int4*)(sc + nreq * 24);
+  a.dummy = sc;
+  a.sp = (int4*)(sc + dummy_bytes);
+  a.sd_t = (double*)(sc + dummy_bytes + nreq * 16);
+  a.sd_m = (int4*)(sc + dummy_bytes + nreq * 24);
   a.flag = sim->d_flag;
   if (sim->timing) {
     if ((st = collect_timing(sim)) != RT_OK) return st;
     if ((e = hipEventRecord(sim->t0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   }
+  // Kernel classes with work, largest first; more than one run side by side
+  // on internal streams forked from and joined back into `stream`.
+  std::vector<int> act;
+  std::vector<double> cost(ncls, 0.0);
   for (int c = 0; c < ncls; ++c) {
     if (buckets[c].empty()) continue;
+    act.push_back(c);
+    for (int32_t r : buckets[c]) cost[c] += (double)(off[r + 1] - off[r]) * rt::sim_class(c).S;
+  }
+  std::stable_sort(act.begin(), act.end(), [&](int x, int y) { return cost[x] > cost[y]; });
+  if (act.size() > 1) {
+    while (sim->lanes.size() < act.size()) {
+      hipStream_t l = nullptr;
+      hipEvent_t j = nullptr;
+      if ((e = hipStreamCreateWithFlags(&l, hipStreamNonBlocking)) != hipSuccess) return hip_fail(e, "hipStreamCreate");
+      sim->lanes.push_back(l);
+      if ((e = hipEventCreateWithFlags(&j, hipEventDisableTiming)) != hipSuccess) return hip_fail(e, "hipEventCreate");
+      sim->joins.push_back(j);
+    }
+    if (!sim->fork && (e = hipEventCreateWithFlags(&sim->fork, hipEventDisableTiming)) != hipSuccess)
+      return hip_fail(e, "hipEventCreate");
+    if ((e = hipEventRecord(sim->fork, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
+  for (size_t k = 0; k < act.size(); ++k) {
+    const int c = act[k];
     a.work = sim->d_work + start[c];
     a.n_work = (int64_t)buckets[c].size();
-    if ((e = rt::launch_sim(rt::sim_class(c), a, stream)) != hipSuccess) return hip_fail(e, "launch(sim)");
+    hipStream_t where = stream;
+    if (act.size() > 1) {
+      where = sim->lanes[k];
+      if ((e = hipStreamWaitEvent(where, sim->fork, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+    }
+    if ((e = rt::launch_sim(rt::sim_class(c), a, where)) != hipSuccess) return hip_fail(e, "launch(sim)");
+    if (act.size() > 1) {
+      if ((e = hipEventRecord(sim->joins[k], where)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+      if ((e = hipStreamWaitEvent(stream, sim->joins[k], 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+    }
   }
   if (sim->timing) {
     if ((e = hipEventRecord(sim->t1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");

@@ -22,7 +22,7 @@ struct DevPoint {
   int64_t slo_ttft[kMaxClasses], slo_tpot[kMaxClasses];
 };
 
-enum : uint32_t { kFlagRejected = 1u, kFlagBadTrace = 2u };
+enum : uint32_t { kFlagRejected = 1u, kFlagBadTrace = 2u, kFlagTimeRange = 4u };
 
 // Arguments of the replica-simulation kernels.
 struct SimArgs {
@@ -42,12 +42,14 @@ struct SimArgs {
   int64_t* span;
   // Successor records of the per-instance FIFOs (one slot per request and
   // pool, indexed by the global request index of the predecessor).
-  int64_t* sp_t;
-  int2* sp_m;  // {successor index within the replica, prompt tokens}
-  int64_t* sd_t;
-  int4* sd_m;  // {successor index, cache tokens p+o, priced tokens o^, 0}
+  int4* sp;       // prefill: {release (double bits lo, hi), successor index, prompt tokens}
+  double* sd_t;   // decode release time
+  int4* sd_m;     // decode: {successor index, cache tokens p+o, ledger tokens o^, 0}
+  char* dummy;    // kDummyLanes private 64-byte slots (writes with nothing to write)
   uint32_t* flag;
 };
+
+constexpr int kDummyLanes = 1 << 16;
 
 // Kernel classes: lanes per replica S (a power of two; S > 64 spans S/64
 // waves of one workgroup) and instances per lane for each pool.

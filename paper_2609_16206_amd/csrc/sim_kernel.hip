@@ -12,52 +12,100 @@
 // holds the minimum cost also holds the lowest index.  All per-instance state
 // (busy-until, queue, cache occupancy, ledger tokens, FIFO head) is in
 // registers; every lane of a segment computes the per-request quantities
-// redundantly, so no broadcast is needed for them.
+// redundantly.  Segment reductions use DPP lane permutations within 16-lane
+// rows and readlane across rows (no LDS round trip); S > 64 combines the
+// per-wave winners through LDS with one barrier per step.
+//
+// Number representation.  Simulated times (ns) and token totals are integers;
+// inside the kernel they are held as doubles, which represent every integer
+// below 2^53 exactly, so sums, differences and maxima are exact and a
+// double-to-float conversion rounds the exact integer to nearest even, the
+// same float as an int64-to-float conversion.  On gfx950 these are single
+// full-rate f64 instructions, where int64 arithmetic takes 2-3 instructions
+// and an int64-to-float conversion a long sequence.  Times at or beyond 2^53
+// ns (104 days) set a flag bit.
 //
 // FIFO of in-flight requests per instance.  Service is in admission order,
 // so each instance releases its requests in admission order and only the
 // head's release time matters for retiring.  The list is kept as successor
 // records in HBM scratch: when request y is appended behind x, y's record
 // (release time, index, cache tokens, ledger tokens) is stored in x's slot.
-// The head and the second element are cached in registers; after a pop the
-// record behind the new head is loaded into a pending register set and
-// merged at the start of the next step, so a single pop per step never waits
-// for memory.  The same lane always writes and reads an instance's slots.
+// The head and the second element live in registers; a pop promotes the
+// second element and loads the record behind it into a pending register set
+// that is merged at the top of the next step.
 //
-// Arithmetic: the cost is evaluated exactly as the equation is written, left
+// Memory ordering within a step (one wave).  On gfx9 stores and loads share
+// one counter, so a wait for a load also waits for every older store.  A step
+// therefore places its one wait before its stores:
+//   1. the current request (prefetched during the previous step); prefetch
+//      the next one (index clamped into the replica);
+//   2. release: at most one pop per instance, whose successor load is issued
+//      unconditionally (from the wave's dummy slot when nothing was popped),
+//      so that it lands in its own registers with no control-flow merge;
+//      more pops at one instance in one step take a rare slow path that
+//      waits;
+//   3. score, argmin, serve (registers only);
+//   4. merge the successor records loaded in 2 (the wait: those loads, and
+//      stores of the previous step, which by now have long completed);
+//   5. stores (outputs, FIFO appends) by the lanes that own them.
+// The same lane always writes and reads an instance's slots, in program
+// order, so a store is visible to every later load of that slot.
+//
+// Arithmetic of the cost: evaluated exactly as the equation is written, left
 // to right in float32, one rounding per operation (built with
-// -ffp-contract=off); integer-to-float conversions round to nearest even.
+// -ffp-contract=off).
 #include "rt_internal.h"
 
 namespace rt {
 namespace {
 
-struct Rec {
-  int64_t t;    // release time
-  int32_t idx;  // index within the replica
-  int32_t fp;   // cache tokens held until release
-  int32_t pt;   // tokens the ledger prices
-};
+constexpr double kTwo32 = 4294967296.0;
+constexpr double kTimeLimit = 9007199254740992.0;  // 2^53
+
+// int64 -> double, exact for |x| < 2^53.
+__device__ __forceinline__ double i64_to_f64(int64_t x) {
+  return __builtin_fma((double)(int32_t)(x >> 32), kTwo32, (double)(uint32_t)(uint64_t)x);
+}
+
+// double holding an integer in [0, 2^53) -> int64.
+__device__ __forceinline__ int64_t f64_to_i64(double x) {
+  const double hi = __builtin_trunc(x * (1.0 / kTwo32));
+  const double lo = __builtin_fma(-hi, kTwo32, x);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
 
 // Per-instance state.  Plain scalars only, copied field by field with value
 // selects, so that everything stays in registers.
 struct Inst {
-  int64_t busy;  // end of everything admitted so far
-  int64_t kv;    // cache tokens in flight
-  int64_t pend;  // ledger tokens in flight
-  int32_t q;     // requests in flight
-  int32_t tail;  // index of the last admitted request
+  double busy;  // end of everything admitted so far
+  double kv;    // cache tokens in flight
+  double pend;  // ledger tokens in flight
+  int32_t q;    // requests in flight
+  int32_t tail; // index of the last admitted request
   // head of the FIFO (valid if q >= 1)
-  int64_t h_t;
+  double h_t;
   int32_t h_idx, h_fp, h_pt;
   // second element (valid if q >= 2 and lp == 0)
-  int64_t n_t;
+  double n_t;
   int32_t n_idx, n_fp, n_pt;
   // load target for the second element (valid if lp != 0)
-  int64_t l_t;
+  double l_t;
   int32_t l_idx, l_fp, l_pt;
   int32_t lp;
 };
+
+__device__ __forceinline__ void init_inst(Inst& s) {
+  s.busy = 0.0;
+  s.kv = 0.0;
+  s.pend = 0.0;
+  s.q = 0;
+  s.tail = -1;
+  s.h_t = s.n_t = s.l_t = 0.0;
+  s.h_idx = s.h_fp = s.h_pt = 0;
+  s.n_idx = s.n_fp = s.n_pt = 0;
+  s.l_idx = s.l_fp = s.l_pt = 0;
+  s.lp = 0;
+}
 
 __device__ __forceinline__ void merge_pending(Inst& s) {
   const bool c = s.lp != 0;
@@ -68,39 +116,11 @@ __device__ __forceinline__ void merge_pending(Inst& s) {
   s.lp = 0;
 }
 
-__device__ __forceinline__ int64_t shfl64(int64_t v, int src) {
-  int lo = __shfl((int)(uint32_t)(uint64_t)v, src, 64);
-  int hi = __shfl((int)(uint32_t)((uint64_t)v >> 32), src, 64);
-  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
-}
-
-template <int S>
-__device__ __forceinline__ uint32_t seg_min(uint32_t v) {
-#pragma unroll
-  for (int m = 1; m < S && m < 64; m <<= 1) v = min(v, (uint32_t)__shfl_xor((int)v, m, 64));
-  return v;
-}
-
-template <int S>
-__device__ __forceinline__ int32_t seg_max_i32(int32_t v) {
-#pragma unroll
-  for (int m = 1; m < S && m < 64; m <<= 1) v = max(v, __shfl_xor(v, m, 64));
-  return v;
-}
-
-__device__ __forceinline__ int32_t wave_max_i32(int32_t v) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) v = max(v, __shfl_xor(v, m, 64));
-  return v;
-}
-
-// Pop the head of an instance's FIFO (caller checked q >= 1).  kDec selects
-// the decode record layout {idx, cache tokens, ledger tokens, 0}; prefill
-// records are {idx, prompt tokens} (cache and ledger tokens are both p).
-__device__ __forceinline__ void pop_common(Inst& s) {
-  s.q -= 1;
-  s.kv -= s.h_fp;
-  s.pend -= s.h_pt;
+// Materializes the merged second element here, ahead of every later memory
+// instruction (an empty volatile asm that reads the registers and clobbers
+// memory), so that the wait for its load is not pushed past the stores.
+__device__ __forceinline__ void pin_record(const Inst& s) {
+  asm volatile("" ::"v"(s.n_t), "v"(s.n_idx), "v"(s.n_fp), "v"(s.n_pt) : "memory");
 }
 
 // The successor slot read after a pop is clamped into the replica's range:
@@ -112,50 +132,77 @@ __device__ __forceinline__ int64_t slot_of(int64_t base, int32_t idx, int32_t R)
   return base + idx;
 }
 
-__device__ __forceinline__ void pop_pre(Inst& s, const int64_t* __restrict__ succ_t,
-                                        const int2* __restrict__ succ_m, int64_t base, int32_t R) {
-  pop_common(s);
-  if (s.q >= 1) {
-    merge_pending(s);  // only does work on a second pop within one step
-    s.h_t = s.n_t;
-    s.h_idx = s.n_idx;
-    s.h_fp = s.n_fp;
-    s.h_pt = s.n_pt;
-    if (s.q >= 2) {
-      const int64_t g = slot_of(base, s.h_idx, R);
-      const int2 m = succ_m[g];
-      s.l_t = succ_t[g];
-      s.l_idx = m.x;
-      s.l_fp = m.y;
-      s.l_pt = m.y;
-      s.lp = 1;
+// Records: prefill {release (double bits), successor index, prompt tokens}
+// in one 16-byte unit; decode {release} in 8 bytes plus {successor index,
+// cache tokens p+o, ledger tokens o^, 0} in 16.
+__device__ __forceinline__ void read_pre(const int4& m, double& t, int32_t& idx, int32_t& fp, int32_t& pt) {
+  t = __hiloint2double(m.y, m.x);
+  idx = m.z;
+  fp = m.w;
+  pt = m.w;
+}
+
+// Fast-path pop, applied with selects when `pp`: the second element becomes
+// the head.  The record behind the new head is then loaded unconditionally
+// (from `dummy` when there is no such record) straight into the pending set.
+template <bool kDec>
+__device__ __forceinline__ void pop_fast(Inst& s, bool pp, const SimArgs& a, const char* dummy, int64_t base,
+                                         int32_t R) {
+  s.q -= pp ? 1 : 0;
+  s.kv -= pp ? (double)s.h_fp : 0.0;
+  s.pend -= pp ? (double)s.h_pt : 0.0;
+  s.h_t = pp ? s.n_t : s.h_t;
+  s.h_idx = pp ? s.n_idx : s.h_idx;
+  s.h_fp = pp ? s.n_fp : s.h_fp;
+  s.h_pt = pp ? s.n_pt : s.h_pt;
+  const bool ld = pp && s.q >= 2;
+  const int64_t g = slot_of(base, s.h_idx, R);
+  if constexpr (kDec) {
+    const double* pt = ld ? a.sd_t + g : reinterpret_cast<const double*>(dummy);
+    const int4* pm = ld ? a.sd_m + g : reinterpret_cast<const int4*>(dummy + 16);
+    s.l_t = *pt;
+    const int4 m = *pm;
+    s.l_idx = m.x;
+    s.l_fp = m.y;
+    s.l_pt = m.z;
+  } else {
+    const int4* pm = ld ? a.sp + g : reinterpret_cast<const int4*>(dummy);
+    read_pre(*pm, s.l_t, s.l_idx, s.l_fp, s.l_pt);
+  }
+  s.lp = ld ? 1 : 0;
+}
+
+// Slow-path pop (a further completion at the same instance within one step):
+// merges what is pending, pops, and reads the next record synchronously.
+template <bool kDec>
+__device__ __forceinline__ void pop_slow(Inst& s, const SimArgs& a, int64_t base, int32_t R) {
+  merge_pending(s);
+  s.q -= 1;
+  s.kv -= (double)s.h_fp;
+  s.pend -= (double)s.h_pt;
+  s.h_t = s.n_t;
+  s.h_idx = s.n_idx;
+  s.h_fp = s.n_fp;
+  s.h_pt = s.n_pt;
+  if (s.q >= 2) {
+    const int64_t g = slot_of(base, s.h_idx, R);
+    if constexpr (kDec) {
+      s.n_t = a.sd_t[g];
+      const int4 m = a.sd_m[g];
+      s.n_idx = m.x;
+      s.n_fp = m.y;
+      s.n_pt = m.z;
+    } else {
+      read_pre(a.sp[g], s.n_t, s.n_idx, s.n_fp, s.n_pt);
     }
   }
 }
 
-__device__ __forceinline__ void pop_dec(Inst& s, const int64_t* __restrict__ succ_t,
-                                        const int4* __restrict__ succ_m, int64_t base, int32_t R) {
-  pop_common(s);
-  if (s.q >= 1) {
-    merge_pending(s);
-    s.h_t = s.n_t;
-    s.h_idx = s.n_idx;
-    s.h_fp = s.n_fp;
-    s.h_pt = s.n_pt;
-    if (s.q >= 2) {
-      const int64_t g = slot_of(base, s.h_idx, R);
-      const int4 m = succ_m[g];
-      s.l_t = succ_t[g];
-      s.l_idx = m.x;
-      s.l_fp = m.y;
-      s.l_pt = m.z;
-      s.lp = 1;
-    }
-  }
-}
-
-// Append request r (release t, index idx, cache tokens fp, ledger tokens pt).
-__device__ __forceinline__ void append_common(Inst& s, int64_t t, int32_t idx, int32_t fp, int32_t pt) {
+// Append a request (release t, index idx, cache tokens fp, ledger tokens
+// pt).  Returns the scratch slot whose successor record must be stored (the
+// previous tail's), or -1.
+__device__ __forceinline__ int64_t append(Inst& s, double t, int32_t idx, int32_t fp, int32_t pt, int64_t base) {
+  const int64_t slot = s.q >= 1 ? base + s.tail : -1;
   const bool first = s.q == 0, second = s.q == 1;
   s.h_t = first ? t : s.h_t;
   s.h_idx = first ? idx : s.h_idx;
@@ -167,59 +214,106 @@ __device__ __forceinline__ void append_common(Inst& s, int64_t t, int32_t idx, i
   s.n_pt = second ? pt : s.n_pt;
   s.tail = idx;
   s.q += 1;
-  s.kv += fp;
-  s.pend += pt;
-}
-
-__device__ __forceinline__ void append_pre(Inst& s, int64_t t, int32_t idx, int32_t p, int64_t* __restrict__ succ_t,
-                                           int2* __restrict__ succ_m, int64_t base) {
-  if (s.q >= 1) {
-    succ_t[base + s.tail] = t;
-    succ_m[base + s.tail] = make_int2(idx, p);
-  }
-  append_common(s, t, idx, p, p);
-}
-
-__device__ __forceinline__ void append_dec(Inst& s, int64_t t, int32_t idx, int32_t fp, int32_t pt,
-                                           int64_t* __restrict__ succ_t, int4* __restrict__ succ_m, int64_t base) {
-  if (s.q >= 1) {
-    succ_t[base + s.tail] = t;
-    succ_m[base + s.tail] = make_int4(idx, fp, pt, 0);
-  }
-  append_common(s, t, idx, fp, pt);
-}
-
-__device__ __forceinline__ void init_inst(Inst& s) {
-  s.busy = 0;
-  s.kv = 0;
-  s.pend = 0;
-  s.q = 0;
-  s.tail = -1;
-  s.h_t = s.n_t = s.l_t = 0;
-  s.h_idx = s.h_fp = s.h_pt = 0;
-  s.n_idx = s.n_fp = s.n_pt = 0;
-  s.l_idx = s.l_fp = s.l_pt = 0;
-  s.lp = 0;
+  s.kv += (double)fp;
+  s.pend += (double)pt;
+  return slot;
 }
 
 // The cost equation for one candidate (Section III-A), in written order.
+// `occ_need` is the exact cache occupancy after admission.
 __device__ __forceinline__ float cost_eq(float w_b, float rho, float w_q, float backlog_s, float work,
-                                         float sg, int64_t kv, int64_t need, float inv_cap, int32_t q) {
-  const float press = (float)(kv + need) * inv_cap;
+                                         float sg, double occ_need, float inv_cap, int32_t q) {
+  const float press = (float)occ_need * inv_cap;
   const float load = w_b * backlog_s * sg;
   const float size = work * (1.0f + rho * press) * sg;
   return load + size + w_q * (float)q;
 }
 
-struct Winner {
-  int32_t idx;
-  int64_t busy;
-};
+// ---------------------------------------------------------------------------
+// Segment collectives over aligned groups of S lanes.  Within a 16-lane row:
+// quad_perm xor 1, xor 2, then half-row mirror and row mirror (each step
+// pairs every lane with one from the other half of its group, so after
+// log2(S) steps every lane holds the group result).  Across rows: readlane
+// of each row.  For S > 64 these reduce over the wave.
+// ---------------------------------------------------------------------------
+template <int C>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, C, 0xF, 0xF, true);
+}
+
+__device__ __forceinline__ uint32_t rl(uint32_t v, int lane) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+
+template <int S>
+__device__ __forceinline__ uint32_t seg_min(uint32_t v, int lane) {
+  if constexpr (S >= 2) v = min(v, dpp<0xB1>(v));
+  if constexpr (S >= 4) v = min(v, dpp<0x4E>(v));
+  if constexpr (S >= 8) v = min(v, dpp<0x141>(v));
+  if constexpr (S >= 16) v = min(v, dpp<0x140>(v));
+  if constexpr (S == 32) {
+    const uint32_t a = min(rl(v, 0), rl(v, 16)), b = min(rl(v, 32), rl(v, 48));
+    v = lane < 32 ? a : b;
+  } else if constexpr (S >= 64) {
+    v = min(min(rl(v, 0), rl(v, 16)), min(rl(v, 32), rl(v, 48)));
+  }
+  return v;
+}
+
+template <int S>
+__device__ __forceinline__ uint32_t seg_or(uint32_t v, int lane) {
+  if constexpr (S >= 2) v |= dpp<0xB1>(v);
+  if constexpr (S >= 4) v |= dpp<0x4E>(v);
+  if constexpr (S >= 8) v |= dpp<0x141>(v);
+  if constexpr (S >= 16) v |= dpp<0x140>(v);
+  if constexpr (S == 32) {
+    const uint32_t a = rl(v, 0) | rl(v, 16), b = rl(v, 32) | rl(v, 48);
+    v = lane < 32 ? a : b;
+  } else if constexpr (S >= 64) {
+    v = (rl(v, 0) | rl(v, 16)) | (rl(v, 32) | rl(v, 48));
+  }
+  return v;
+}
+
+// Maximum over the whole wave of non-negative values.
+__device__ __forceinline__ int32_t wave_max_nonneg(int32_t v) {
+  uint32_t u = (uint32_t)v;
+  u = max(u, dpp<0xB1>(u));
+  u = max(u, dpp<0x4E>(u));
+  u = max(u, dpp<0x141>(u));
+  u = max(u, dpp<0x140>(u));
+  u = max(max(rl(u, 0), rl(u, 16)), max(rl(u, 32), rl(u, 48)));
+  return (int32_t)u;
+}
+
+// Broadcast a double from the one lane of each segment where `own` holds
+// (every other lane contributes 0 bits to an OR).
+template <int S>
+__device__ __forceinline__ double seg_bcast_f64(double v, bool own, int lane) {
+  const int lo = own ? __double2loint(v) : 0;
+  const int hi = own ? __double2hiint(v) : 0;
+  return __hiloint2double((int)seg_or<S>((uint32_t)hi, lane), (int)seg_or<S>((uint32_t)lo, lane));
+}
+
+// Lowest lane (relative to the segment, or to the wave for S >= 64) of each
+// segment where `pred` holds.
+template <int S>
+__device__ __forceinline__ int32_t seg_first(bool pred, int lane) {
+  const uint64_t b = __ballot(pred);
+  if constexpr (S >= 64) {
+    return __ffsll((unsigned long long)b) - 1;
+  } else {
+    const uint32_t half = lane < 32 ? (uint32_t)b : (uint32_t)(b >> 32);
+    const int sh = (lane & 31) & ~(S - 1);
+    const uint32_t mask = (S == 32) ? 0xffffffffu : ((1u << (S & 31)) - 1u);
+    return __ffs((half >> sh) & mask) - 1;
+  }
+}
 
 struct Partial {
-  uint32_t key;
-  int32_t idx;
-  int64_t busy;
+  uint32_t key_pre, key_dec;
+  int32_t idx_pre, idx_dec;
+  double busy_pre;
 };
 
 template <int S, int MP, int MD>
@@ -232,16 +326,14 @@ __global__ void __launch_bounds__(S > 64 ? S : 256) sim_kernel(SimArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   int sl;        // lane within the replica's segment
   int64_t item;  // position in the work list
-  int seg_base;  // first lane of the segment within the wave
   if constexpr (S <= 64) {
     sl = lane % S;
-    seg_base = lane - sl;
     item = ((int64_t)blockIdx.x * (blockDim.x >> 6) + wave) * kSegs + lane / S;
   } else {
     sl = threadIdx.x;
-    seg_base = 0;
     item = blockIdx.x;
   }
+  const int wl_self = S > 64 ? lane : sl;  // lane index seg_first reports
   const bool live = item < a.n_work;
   const int rep = live ? a.work[item] : 0;
   const int64_t base = live ? a.offsets[rep] : 0;
@@ -255,10 +347,10 @@ __global__ void __launch_bounds__(S > 64 ? S : 256) sim_kernel(SimArgs a) {
   float sigma[kMaxClasses];
 #pragma unroll
   for (int c = 0; c < kMaxClasses; ++c) sigma[c] = pp.sigma[c];
-  const int64_t pre_base_ns = pp.pre_base_ns, pre_tok_ns = pp.pre_tok_ns;
-  const int64_t dec_tok_ns = pp.dec_tok_ns, xfer_tok_ns = pp.xfer_tok_ns;
+  const double pre_base_ns = (double)pp.pre_base_ns, pre_tok_ns = (double)pp.pre_tok_ns;
+  const double dec_tok_ns = (double)pp.dec_tok_ns, xfer_tok_ns = (double)pp.xfer_tok_ns;
 
-  __shared__ Partial part[S > 64 ? 2 * 2 * kW : 1];
+  __shared__ Partial part[S > 64 ? 2 * kW : 1];
 
   Inst pre[MP], dec[MD];
 #pragma unroll
@@ -266,11 +358,12 @@ __global__ void __launch_bounds__(S > 64 ? S : 256) sim_kernel(SimArgs a) {
 #pragma unroll
   for (int m = 0; m < MD; ++m) init_inst(dec[m]);
 
-  int32_t Rmax;
-  if constexpr (S <= 64)
-    Rmax = wave_max_i32(R);
-  else
-    Rmax = R;  // one replica per workgroup
+  // steps of this wave: the longest replica among its segments
+  const int32_t Rmax = S <= 64 ? wave_max_nonneg(R) : R;
+  // the wave's 64-byte dummy slot (see the memory-ordering note); every lane
+  // of the wave reads the same address, which costs one memory request
+  char* const dummy =
+      a.dummy + (size_t)(((blockIdx.x * blockDim.x + threadIdx.x) >> 6) & (kDummyLanes / 64 - 1)) * 64;
 
   // Prefetched features of the next request.
   int64_t nx_arr = 0;
@@ -287,13 +380,18 @@ __global__ void __launch_bounds__(S > 64 ? S : 256) sim_kernel(SimArgs a) {
   bool have_arr = false;
   int32_t rr_pre = 0, rr_dec = 0;  // round-robin counters: t mod P, t mod D
 
+  uint32_t flag = 0;  // data-error bits, published once at the end
+
   for (int32_t t = 0; t < Rmax; ++t) {
+    // 1. the current request; prefetch the next (index clamped into the
+    // replica, so the same loads are issued at every step)
     const bool act = t < R;
-    const int64_t now = nx_arr;
+    const int64_t arr = nx_arr;
     const int32_t p = nx_p, o = nx_o, oh = nx_oh;
     const uint32_t c = nx_c;
-    if (t + 1 < R) {
-      const int64_t g = base + t + 1;
+    {
+      const int32_t tn = t + 1 < R ? t + 1 : (R > 0 ? R - 1 : 0);
+      const int64_t g = base + tn;
       nx_arr = a.arrival[g];
       nx_p = a.plen[g];
       nx_o = a.olen[g];
@@ -301,170 +399,218 @@ __global__ void __launch_bounds__(S > 64 ? S : 256) sim_kernel(SimArgs a) {
       nx_c = a.cls[g];
     }
     const bool bad = act && (p < 1 || o < 1 || oh < 1 || (int64_t)p + o > INT32_MAX ||
-                             (int64_t)p + oh > INT32_MAX || c >= (uint32_t)ncls || now < 0 ||
-                             (have_arr && now < last_arr));
+                             (int64_t)p + oh > INT32_MAX || c >= (uint32_t)ncls || arr < 0 ||
+                             (have_arr && arr < last_arr));
     const bool go = act && !bad;
     if (go) {
-      last_arr = now;
+      last_arr = arr;
       have_arr = true;
     }
+    const double now = i64_to_f64(arr);
 
-    // Merge the successor records loaded during the previous step.
+    // 2. release everything that finished at or before now: one pop per
+    // instance on the fast path; further pops (several completions between
+    // two arrivals at one instance) on the slow path, which waits.
 #pragma unroll
-    for (int m = 0; m < MP; ++m) merge_pending(pre[m]);
+    for (int m = 0; m < MP; ++m)
+      pop_fast<false>(pre[m], go && pre[m].q > 0 && pre[m].h_t <= now, a, dummy + 32, base, R);
 #pragma unroll
-    for (int m = 0; m < MD; ++m) merge_pending(dec[m]);
-
-    // 1. Release everything that finished at or before now.
-    while (true) {
-      bool want = false;
+    for (int m = 0; m < MD; ++m)
+      pop_fast<true>(dec[m], go && dec[m].q > 0 && dec[m].h_t <= now, a, dummy + 32, base, R);
+    {
+      bool more = false;
 #pragma unroll
-      for (int m = 0; m < MP; ++m) want |= go && pre[m].q > 0 && pre[m].h_t <= now;
+      for (int m = 0; m < MP; ++m) more |= go && pre[m].q > 0 && pre[m].h_t <= now;
 #pragma unroll
-      for (int m = 0; m < MD; ++m) want |= go && dec[m].q > 0 && dec[m].h_t <= now;
-      if (!__any(want)) break;
+      for (int m = 0; m < MD; ++m) more |= go && dec[m].q > 0 && dec[m].h_t <= now;
+      while (__any(more)) {
 #pragma unroll
-      for (int m = 0; m < MP; ++m)
-        if (go && pre[m].q > 0 && pre[m].h_t <= now) pop_pre(pre[m], a.sp_t, a.sp_m, base, R);
+        for (int m = 0; m < MP; ++m)
+          if (go && pre[m].q > 0 && pre[m].h_t <= now) pop_slow<false>(pre[m], a, base, R);
 #pragma unroll
-      for (int m = 0; m < MD; ++m)
-        if (go && dec[m].q > 0 && dec[m].h_t <= now) pop_dec(dec[m], a.sd_t, a.sd_m, base, R);
+        for (int m = 0; m < MD; ++m)
+          if (go && dec[m].q > 0 && dec[m].h_t <= now) pop_slow<true>(dec[m], a, base, R);
+        more = false;
+#pragma unroll
+        for (int m = 0; m < MP; ++m) more |= go && pre[m].q > 0 && pre[m].h_t <= now;
+#pragma unroll
+        for (int m = 0; m < MD; ++m) more |= go && dec[m].q > 0 && dec[m].h_t <= now;
+        // Leave the slow path with nothing of its own in flight, so that the
+        // loads and register writes after it keep exact wait counts.
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+      }
     }
 
-    // 2. Keys of every candidate under the point's policy.
+    // 3a. keys of every candidate under the point's policy
     float sg = sigma[0];
 #pragma unroll
     for (int k = 1; k < kMaxClasses; ++k) sg = (c == (uint32_t)k) ? sigma[k] : sg;
     const float work_pre = w_s * (float)p * tau_pre;
     const float work_dec = w_s * (float)oh * tau_dec;
-    const int64_t need_pre = p;
-    const int64_t need_dec = (int64_t)p + oh;
+    const double need_pre = (double)p;
+    const double need_dec = (double)p + (double)oh;
 
     uint32_t bk_pre = 0xffffffffu, bk_dec = 0xffffffffu;
-    int32_t bj_pre = 0, bj_dec = 0;
-    int64_t bb_pre = 0, bb_dec = 0;
+    int32_t bm_pre = 0, bm_dec = 0;
+    double bb_pre = 0.0;
 #pragma unroll
     for (int m = 0; m < MP; ++m) {
       const int j = sl * MP + m;
-      uint32_t key;
-      if (policy == 0) {
-        float bl;
-        if (mode == 0) {
-          int64_t d = pre[m].busy - now;
-          d = d < 0 ? 0 : d;
-          bl = (float)d * 1e-9f;
-        } else {
-          bl = tau_pre * (float)pre[m].pend + pre_base * (float)pre[m].q;
-        }
-        key = cost_key(cost_eq(w_b, rho, w_q, bl, work_pre, sg, pre[m].kv, need_pre, inv_pre, pre[m].q));
-      } else if (policy == 2) {
-        key = (uint32_t)pre[m].q;
-      } else {
-        key = (j == rr_pre) ? 0u : 1u;
-      }
+      const float bl = mode == 0 ? (float)__builtin_fmax(pre[m].busy - now, 0.0) * 1e-9f
+                                 : tau_pre * (float)pre[m].pend + pre_base * (float)pre[m].q;
+      uint32_t key = cost_key(cost_eq(w_b, rho, w_q, bl, work_pre, sg, pre[m].kv + need_pre, inv_pre, pre[m].q));
+      key = policy == 2 ? (uint32_t)pre[m].q : key;
+      key = policy == 1 ? (j == rr_pre ? 0u : 1u) : key;
       key = (go && j < P) ? key : 0xffffffffu;
       if (key < bk_pre) {
         bk_pre = key;
-        bj_pre = j;
+        bm_pre = m;
         bb_pre = pre[m].busy;
       }
     }
 #pragma unroll
     for (int m = 0; m < MD; ++m) {
       const int j = sl * MD + m;
-      uint32_t key;
-      if (policy == 0) {
-        float bl;
-        if (mode == 0) {
-          int64_t d = dec[m].busy - now;
-          d = d < 0 ? 0 : d;
-          bl = (float)d * 1e-9f;
-        } else {
-          bl = tau_dec * (float)dec[m].pend;
-        }
-        key = cost_key(cost_eq(w_b, rho, w_q, bl, work_dec, sg, dec[m].kv, need_dec, inv_dec, dec[m].q));
-      } else if (policy == 2) {
-        key = (uint32_t)dec[m].q;
-      } else {
-        key = (j == rr_dec) ? 0u : 1u;
-      }
+      const float bl = mode == 0 ? (float)__builtin_fmax(dec[m].busy - now, 0.0) * 1e-9f
+                                 : tau_dec * (float)dec[m].pend;
+      uint32_t key = cost_key(cost_eq(w_b, rho, w_q, bl, work_dec, sg, dec[m].kv + need_dec, inv_dec, dec[m].q));
+      key = policy == 2 ? (uint32_t)dec[m].q : key;
+      key = policy == 1 ? (j == rr_dec ? 0u : 1u) : key;
       key = (go && j < D) ? key : 0xffffffffu;
       if (key < bk_dec) {
         bk_dec = key;
-        bj_dec = j;
-        bb_dec = dec[m].busy;
+        bm_dec = m;
       }
     }
 
-    // 3. Argmin over the segment (lowest index on equal keys).
-    Winner wp, wd;
+    // 3b. argmin per pool over the segment (lowest index on equal keys) and
+    // the prefill winner's busy-until, known to every lane afterwards.
+    int32_t ip, id;
+    double busy_ip;
     {
-      const uint32_t mp = seg_min<S>(bk_pre);
-      const uint32_t md = seg_min<S>(bk_dec);
-      const uint64_t bp = __ballot(bk_pre == mp);
-      const uint64_t bd = __ballot(bk_dec == md);
-      const uint64_t segmask = (S >= 64) ? ~0ull : ((1ull << (S < 64 ? S : 0)) - 1ull);
-      const uint64_t sp = (bp >> seg_base) & segmask;
-      const uint64_t sd = (bd >> seg_base) & segmask;
-      const int src_p = seg_base + (__ffsll((unsigned long long)sp) - 1);
-      const int src_d = seg_base + (__ffsll((unsigned long long)sd) - 1);
-      wp.idx = __shfl(bj_pre, src_p, 64);
-      wd.idx = __shfl(bj_dec, src_d, 64);
-      wp.busy = shfl64(bb_pre, src_p);
-      wd.busy = shfl64(bb_dec, src_d);
+      const uint32_t kp = seg_min<S>(bk_pre, lane);
+      const uint32_t kd = seg_min<S>(bk_dec, lane);
+      const int32_t wl_p = seg_first<S>(bk_pre == kp, lane);
+      const int32_t wl_d = seg_first<S>(bk_dec == kd, lane);
+      const bool own_p = wl_self == wl_p;
+      const bool own_d = wl_self == wl_d;
+      int32_t jp = wl_p * MP, jd = wl_d * MD;
+      if constexpr (MP > 1) jp += (int32_t)seg_or<S>(own_p ? (uint32_t)bm_pre : 0u, lane);
+      if constexpr (MD > 1) jd += (int32_t)seg_or<S>(own_d ? (uint32_t)bm_dec : 0u, lane);
+      double bp = seg_bcast_f64<S>(bb_pre, own_p, lane);
       if constexpr (S > 64) {
-        // Combine the per-wave winners through LDS (double-buffered by step
-        // parity, so one barrier per step suffices).
-        Partial* buf = part + (t & 1) * 2 * kW;
-        if (lane == 0) {
-          buf[wave] = Partial{mp, wp.idx, wp.busy};
-          buf[kW + wave] = Partial{md, wd.idx, wd.busy};
-        }
+        jp += wave * 64 * MP;
+        jd += wave * 64 * MD;
+        // combine the per-wave winners through LDS (double-buffered by step
+        // parity: one barrier per step)
+        Partial* buf = part + (t & 1) * kW;
+        if (lane == 0) buf[wave] = Partial{kp, kd, jp, jd, bp};
         __syncthreads();
-        Partial bp0 = buf[0], bd0 = buf[kW];
+        Partial w0 = buf[0];
 #pragma unroll
         for (int w = 1; w < kW; ++w) {
-          const Partial x = buf[w], y = buf[kW + w];
-          if (x.key < bp0.key) bp0 = x;  // waves hold increasing index ranges
-          if (y.key < bd0.key) bd0 = y;
+          const Partial x = buf[w];  // waves hold increasing index ranges
+          if (x.key_pre < w0.key_pre) {
+            w0.key_pre = x.key_pre;
+            w0.idx_pre = x.idx_pre;
+            w0.busy_pre = x.busy_pre;
+          }
+          if (x.key_dec < w0.key_dec) {
+            w0.key_dec = x.key_dec;
+            w0.idx_dec = x.idx_dec;
+          }
         }
-        wp = Winner{bp0.idx, bp0.busy};
-        wd = Winner{bd0.idx, bd0.busy};
+        jp = w0.idx_pre;
+        jd = w0.idx_dec;
+        bp = w0.busy_pre;
       }
+      ip = jp;
+      id = jd;
+      busy_ip = bp;
     }
 
-    // 4. Serve: prefill, KV transfer, decode, each FIFO in admission order.
-    const int64_t s_pre = pre_base_ns + (int64_t)p * pre_tok_ns;
-    const int64_t s_dec = (int64_t)(o - 1) * dec_tok_ns;
-    const int64_t xfer = (int64_t)p * xfer_tok_ns;
-    const int64_t pf_end = (now > wp.busy ? now : wp.busy) + s_pre;
-    const int64_t kv_at = pf_end + xfer;
-    const int64_t dec_end = (kv_at > wd.busy ? kv_at : wd.busy) + s_dec;
+    // 3c. serve: prefill, KV transfer, decode, each FIFO in admission order
+    // (every product below is an exact integer under the 2^53 limit)
+    const double s_pre = __builtin_fma((double)p, pre_tok_ns, pre_base_ns);
+    const double s_dec = (double)(o - 1) * dec_tok_ns;
+    const double xfer = (double)p * xfer_tok_ns;
+    const double pf_end = __builtin_fmax(now, busy_ip) + s_pre;
+    const double kv_at = pf_end + xfer;
+    int64_t d_out = -1;  // output index this lane writes
+    int32_t d_ipre = 0, d_idec = 0;
+    int64_t d_ttft = 0, d_span = 0;
+    int64_t d_ps = -1;  // prefill successor slot this lane writes, and its record
+    double d_pt = 0.0;
+    int32_t d_pidx = 0, d_pp = 0;
+    int64_t d_ds = -1;  // decode successor slot this lane writes, and its record
+    double d_dt = 0.0;
+    int32_t d_didx = 0, d_dfp = 0, d_dpt = 0;
 #pragma unroll
     for (int m = 0; m < MP; ++m)
-      if (go && sl * MP + m == wp.idx) {
-        append_pre(pre[m], pf_end, t, p, a.sp_t, a.sp_m, base);
+      if (go && sl * MP + m == ip) {
+        d_ps = append(pre[m], pf_end, t, p, p, base);
         pre[m].busy = pf_end;
+        d_pt = pf_end;
+        d_pidx = t;
+        d_pp = p;
       }
 #pragma unroll
     for (int m = 0; m < MD; ++m)
-      if (go && sl * MD + m == wd.idx) {
-        append_dec(dec[m], dec_end, t, p + o, oh, a.sd_t, a.sd_m, base);
+      if (go && sl * MD + m == id) {
+        const double dec_end = __builtin_fmax(kv_at, dec[m].busy) + s_dec;
+        d_ds = append(dec[m], dec_end, t, p + o, oh, base);
         dec[m].busy = dec_end;
+        d_dt = dec_end;
+        d_didx = t;
+        d_dfp = p + o;
+        d_dpt = oh;
+        // the decode owner records the outcome
+        d_out = base + t;
+        d_ipre = ip;
+        d_idec = id;
+        d_ttft = f64_to_i64(pf_end - now);
+        d_span = f64_to_i64(dec_end - pf_end);
+        flag |= dec_end >= kTimeLimit ? kFlagTimeRange : 0u;
       }
+    if (bad && sl == 0) {
+      d_out = base + t;
+      d_ipre = d_idec = -1;
+      d_ttft = d_span = -1;
+      flag |= kFlagRejected;
+    }
 
-    // 5. Record the outcome.
-    if (act && sl == 0) {
-      const int64_t g = base + t;
-      a.i_pre[g] = go ? wp.idx : -1;
-      a.i_dec[g] = go ? wd.idx : -1;
-      a.ttft[g] = go ? pf_end - now : -1;
-      a.span[g] = go ? dec_end - pf_end : -1;
-      if (bad) atomicOr(a.flag, kFlagRejected);
+    // 4. the successor records loaded in 2 (the step's one wait).  The
+    // scheduling barriers keep the wait after the step's arithmetic and before
+    // its stores.
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int m = 0; m < MP; ++m) {
+      merge_pending(pre[m]);
+      pin_record(pre[m]);
+    }
+#pragma unroll
+    for (int m = 0; m < MD; ++m) {
+      merge_pending(dec[m]);
+      pin_record(dec[m]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // 5. stores, by the lanes that own them
+    if (d_out >= 0) {
+      a.i_pre[d_out] = d_ipre;
+      a.i_dec[d_out] = d_idec;
+      a.ttft[d_out] = d_ttft;
+      a.span[d_out] = d_span;
+    }
+    if (d_ps >= 0) a.sp[d_ps] = make_int4(__double2loint(d_pt), __double2hiint(d_pt), d_pidx, d_pp);
+    if (d_ds >= 0) {
+      a.sd_t[d_ds] = d_dt;
+      a.sd_m[d_ds] = make_int4(d_didx, d_dfp, d_dpt, 0);
     }
     rr_pre = (rr_pre + 1 == P) ? 0 : rr_pre + 1;
     rr_dec = (rr_dec + 1 == D) ? 0 : rr_dec + 1;
   }
+  if (flag) atomicOr(a.flag, flag);
 }
 
 template <int S, int MP, int MD>
