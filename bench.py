@@ -241,11 +241,22 @@ def main():
     ap.add_argument("--workload", default="cluster", choices=["tiny", "cluster", "sweep", "large", "scorer"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for the CPU baseline")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="first copy MIB MiB device-to-device (a plain copy of known size that scales the "
+                         "hardware byte counters when the run is profiled)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps(dict(error="this build measures one GPU: replicas are independent and would shard "
                                     "across GPUs with no exchange, but only --gpus 1 is run")), flush=True)
         sys.exit(2)
+    if args.calibrate_copy > 0:
+        import torch
+        n = args.calibrate_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     res = bench_scorer(args) if args.workload == "scorer" else bench_sim(args)
     print(json.dumps(res), flush=True)
 

@@ -8,7 +8,7 @@
  *       cost(d) = w_b * backlog(d) * sigma(s_r)
  *               + w_s * o_r * tau_dec * (1 + rho * press+(d)) * sigma(s_r)
  *               + w_q * queue(d),
- *     prefill candidates "analogously" with p_r * tau_pre; the request goes to
+ *     prefill candidates the same way with p_r * tau_pre; the request goes to
  *     the argmin of each pool.
  *   - Algorithm 1: per admission, argmin over the prefill pool, argmin over
  *     the decode pool, prefill, KV transfer, decode, record the outcome.

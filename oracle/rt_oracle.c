@@ -39,8 +39,9 @@ static float cost_eq(const orc_router* rp, float backlog_s, float work, float sg
 }
 
 /* Per-request priced work of a pool: prompt tokens at the prefill price
- * ("scored analogously with p_r tau_pre"), predicted output tokens at the
- * decode price. */
+ * (Section III-A prices prefill candidates like decode ones, with p_r tau_pre
+ * in place of the decode work), predicted output tokens at the decode
+ * price. */
 static float pool_work(const orc_router* rp, int32_t pool, int32_t p, int32_t ohat) {
   if (pool == ORC_PREFILL) return rp->w_s * (float)p * rp->tau_pre_s;
   return rp->w_s * (float)ohat * rp->tau_dec_s;
