@@ -92,7 +92,7 @@ typedef struct {
  * targets).  Service of request r: prefill pre_base_ns + p_r * pre_tok_ns;
  * KV transfer p_r * xfer_tok_ns (a pure delay); decode (o_r - 1) * dec_tok_ns.
  * All >= 0 and <= 2^40; capacities >= 1 (soft: occupancy above capacity is
- * priced, never blocked).  Simulated times must stay below 2^53 ns. */
+ * priced, never blocked).  Simulated times must stay below 2^52 ns. */
 typedef struct {
   int64_t pre_base_ns, pre_tok_ns, dec_tok_ns, xfer_tok_ns;
   int64_t kv_cap_pre, kv_cap_dec;                 /* cache tokens per instance */
@@ -180,8 +180,9 @@ rt_status rt_goodput(const rt_sim* sim, const rt_trace* trace, const rt_sim_out*
  *   bit 0: a request was rejected (length, class or arrival order);
  *   bit 1: rt_goodput met a replica whose offsets or point id are
  *          inconsistent (its goodput is 0 and its met count -1);
- *   bit 2: a simulated time reached 2^53 ns (about 104 days), beyond which
- *          the kernels' exact integer arithmetic no longer holds. */
+ *   bit 2: a simulated time reached 2^52 ns (about 52 days), beyond which
+ *          the kernels' exact integer arithmetic no longer holds (the
+ *          outputs of such a run are not valid). */
 rt_status rt_sim_data_status(rt_sim* sim, void* hip_stream, uint32_t* flags);
 
 /* Measurement hook.  rt_sim_timing(sim, 1) resets the totals and makes every

@@ -74,18 +74,21 @@ rt::DevPoint to_dev(const rt_point& p) {
   d.n_classes = p.n_classes;
   d.policy = p.policy;
   d.mode = p.backlog_mode;
-  d.w_b = p.router.w_b;
-  d.w_s = p.router.w_s;
-  d.w_q = p.router.w_q;
-  d.rho = p.router.rho;
-  d.tau_pre = p.router.tau_pre_s;
-  d.tau_dec = p.router.tau_dec_s;
-  d.pre_base = p.router.pre_base_s;
+  // Adding +0.0f turns a -0.0f weight into +0.0f (and changes nothing else):
+  // with every factor then +0 or positive, no cost is -0 and the kernels can
+  // order costs by their bit patterns without a zero test.
+  d.w_b = p.router.w_b + 0.0f;
+  d.w_s = p.router.w_s + 0.0f;
+  d.w_q = p.router.w_q + 0.0f;
+  d.rho = p.router.rho + 0.0f;
+  d.tau_pre = p.router.tau_pre_s + 0.0f;
+  d.tau_dec = p.router.tau_dec_s + 0.0f;
+  d.pre_base = p.router.pre_base_s + 0.0f;
   // press+ = (occupancy + need) * (1 / capacity): the reciprocal is rounded
   // to float32 once, here.
   d.inv_cap_pre = 1.0f / (float)p.phys.kv_cap_pre;
   d.inv_cap_dec = 1.0f / (float)p.phys.kv_cap_dec;
-  for (int c = 0; c < rt::kMaxClasses; ++c) d.sigma[c] = p.router.sigma[c];
+  for (int c = 0; c < rt::kMaxClasses; ++c) d.sigma[c] = p.router.sigma[c] + 0.0f;
   d.pre_base_ns = p.phys.pre_base_ns;
   d.pre_tok_ns = p.phys.pre_tok_ns;
   d.dec_tok_ns = p.phys.dec_tok_ns;
@@ -97,11 +100,27 @@ rt::DevPoint to_dev(const rt_point& p) {
   return d;
 }
 
-// The cheapest kernel class whose lane segment holds both pools.
+// The scoring path a point's kernels take.
+int point_mode(const rt_point& p) {
+  if (p.policy != RT_POLICY_LEARNED) return rt::kModeBase;
+  return p.backlog_mode == RT_BACKLOG_TRUE ? rt::kModeTrue : rt::kModeProxy;
+}
+
+// The first kernel class (classes are listed in order of preference) that
+// holds both pools of a point: a segment class of the point's mode whose S
+// lanes hold ceil(P / M) prefill lanes and ceil(D / M) decode lanes, else a
+// wide class.
 int pick_class(const rt_point& p) {
+  const int mode = point_mode(p);
   for (int i = 0; i < rt::sim_class_count(); ++i) {
     const rt::SimClass c = rt::sim_class(i);
-    if (p.n_prefill <= c.S * c.MP && p.n_decode <= c.S * c.MD) return i;
+    if (c.kind == rt::kSeg) {
+      if (c.mode != mode) continue;
+      const int lanes = (p.n_prefill + c.MP - 1) / c.MP + (p.n_decode + c.MD - 1) / c.MD;
+      if (lanes <= c.S) return i;
+    } else if (p.n_prefill <= c.S * c.MP && p.n_decode <= c.S * c.MD) {
+      return i;
+    }
   }
   return -1;
 }
@@ -280,10 +299,16 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
     });
 
   hipError_t e;
-  // Scratch: successor records (40 bytes per request) and the dummy slots.
+  // Scratch: successor records (kRecStride bytes per request) and the dummy
+  // slots.
   const size_t nreq = (size_t)trace->n_requests;
+  // (the dummy area also holds the wave-private dummy records at negative
+  // request indices, kDummyLanes / 64 of kRecStride bytes, right before the
+  // records)
   const size_t dummy_bytes = (size_t)rt::kDummyLanes * 64;
-  const size_t need = nreq * 40 + dummy_bytes + 256;
+  static_assert((size_t)rt::kDummyLanes * 64 >= (size_t)(rt::kDummyLanes / 64) * rt::kRecStride * 2,
+                "dummy area too small for the dummy records");
+  const size_t need = nreq * rt::kRecStride + dummy_bytes + 256;
   if (need > sim->scratch_bytes) {
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
     if (sim->d_scratch) (void)hipFree(sim->d_scratch);
@@ -342,9 +367,7 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   a.ttft = out->ttft_ns;
   a.span = out->decode_span_ns;
   a.dummy = sc;
-  a.sp = (int4*)(sc + dummy_bytes);
-  a.sd_t = (double*)(sc + dummy_bytes + nreq * 16);
-  a.sd_m = (int4*)(sc + dummy_bytes + nreq * 24);
+  a.rec = sc + dummy_bytes;
   a.flag = sim->d_flag;
   if (sim->timing) {
     if ((st = collect_timing(sim)) != RT_OK) return st;

@@ -1,0 +1,152 @@
+// Device helpers shared by the replica-simulation kernels: exact integer <->
+// double conversions and collectives over aligned segments of S lanes.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rt {
+
+constexpr double kTwo32 = 4294967296.0;
+constexpr double kTwo52 = 4503599627370496.0;
+// Simulated times stay below 2^52 ns (about 52 days): below it every time,
+// sum and difference the kernels form is an exact integer in a double, and
+// the double-to-int64 conversion below is exact.
+constexpr double kTimeLimit = kTwo52;
+
+// int64 -> double, exact for |x| < 2^53.
+__device__ __forceinline__ double i64_to_f64(int64_t x) {
+  return __builtin_fma((double)(int32_t)(x >> 32), kTwo32, (double)(uint32_t)(uint64_t)x);
+}
+
+// Integer-valued double in [0, 2^52) -> int64: adding 2^52 puts the integer
+// in the low 52 bits of the significand (the exponent field is then fixed).
+__device__ __forceinline__ int64_t f64_to_i64(double x) {
+  const double y = x + kTwo52;
+  const uint32_t hi = (uint32_t)__double2hiint(y) & 0xFFFFFu;
+  return (int64_t)(((uint64_t)hi << 32) | (uint32_t)__double2loint(y));
+}
+
+// Hides a value's provenance from the optimizer (it stays in a VGPR), so that
+// a select on it is not re-associated into a combination of lane masks.
+template <typename T>
+__device__ __forceinline__ T opaque(T x) {
+  asm("" : "+v"(x));
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// Segment collectives over aligned groups of S lanes.  Within a 16-lane row:
+// quad_perm xor 1, xor 2, then half-row mirror and row mirror (each step
+// pairs every lane with one from the other half of its group, so after
+// log2(S) steps every lane holds the group result).  Across rows: readlane
+// of each row.  For S > 64 these reduce over the wave.
+// ---------------------------------------------------------------------------
+template <int C>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, C, 0xF, 0xF, true);
+}
+
+__device__ __forceinline__ uint32_t rl(uint32_t v, int lane) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+
+template <int S>
+__device__ __forceinline__ uint32_t seg_min(uint32_t v, int lane) {
+  if constexpr (S >= 2) v = min(v, dpp<0xB1>(v));
+  if constexpr (S >= 4) v = min(v, dpp<0x4E>(v));
+  if constexpr (S >= 8) v = min(v, dpp<0x141>(v));
+  if constexpr (S >= 16) v = min(v, dpp<0x140>(v));
+  if constexpr (S == 32) {
+    const uint32_t a = min(rl(v, 0), rl(v, 16)), b = min(rl(v, 32), rl(v, 48));
+    v = lane < 32 ? a : b;
+  } else if constexpr (S >= 64) {
+    v = min(min(rl(v, 0), rl(v, 16)), min(rl(v, 32), rl(v, 48)));
+  }
+  return v;
+}
+
+// Two independent segment minima, interleaved so that each DPP step of one
+// fills the other's data-hazard wait.
+template <int S>
+__device__ __forceinline__ void seg_min2(uint32_t& v, uint32_t& w, int lane) {
+  if constexpr (S >= 2) { v = min(v, dpp<0xB1>(v)); w = min(w, dpp<0xB1>(w)); }
+  if constexpr (S >= 4) { v = min(v, dpp<0x4E>(v)); w = min(w, dpp<0x4E>(w)); }
+  if constexpr (S >= 8) { v = min(v, dpp<0x141>(v)); w = min(w, dpp<0x141>(w)); }
+  if constexpr (S >= 16) { v = min(v, dpp<0x140>(v)); w = min(w, dpp<0x140>(w)); }
+  if constexpr (S == 32) {
+    const uint32_t a = min(rl(v, 0), rl(v, 16)), b = min(rl(v, 32), rl(v, 48));
+    const uint32_t c = min(rl(w, 0), rl(w, 16)), d = min(rl(w, 32), rl(w, 48));
+    v = lane < 32 ? a : b;
+    w = lane < 32 ? c : d;
+  } else if constexpr (S >= 64) {
+    v = min(min(rl(v, 0), rl(v, 16)), min(rl(v, 32), rl(v, 48)));
+    w = min(min(rl(w, 0), rl(w, 16)), min(rl(w, 32), rl(w, 48)));
+  }
+}
+
+template <int S>
+__device__ __forceinline__ uint32_t seg_or(uint32_t v, int lane) {
+  if constexpr (S >= 2) v |= dpp<0xB1>(v);
+  if constexpr (S >= 4) v |= dpp<0x4E>(v);
+  if constexpr (S >= 8) v |= dpp<0x141>(v);
+  if constexpr (S >= 16) v |= dpp<0x140>(v);
+  if constexpr (S == 32) {
+    const uint32_t a = rl(v, 0) | rl(v, 16), b = rl(v, 32) | rl(v, 48);
+    v = lane < 32 ? a : b;
+  } else if constexpr (S >= 64) {
+    v = (rl(v, 0) | rl(v, 16)) | (rl(v, 32) | rl(v, 48));
+  }
+  return v;
+}
+
+// Maximum over the whole wave of non-negative values.
+__device__ __forceinline__ int32_t wave_max_nonneg(int32_t v) {
+  uint32_t u = (uint32_t)v;
+  u = max(u, dpp<0xB1>(u));
+  u = max(u, dpp<0x4E>(u));
+  u = max(u, dpp<0x141>(u));
+  u = max(u, dpp<0x140>(u));
+  u = max(max(rl(u, 0), rl(u, 16)), max(rl(u, 32), rl(u, 48)));
+  return (int32_t)u;
+}
+
+// Broadcast a double from the one lane of each segment where `own` holds
+// (every other lane contributes 0 bits to an OR); the two halves are reduced
+// interleaved.
+template <int S>
+__device__ __forceinline__ double seg_bcast_f64(double v, bool own, int lane) {
+  uint32_t lo = own ? (uint32_t)__double2loint(v) : 0u;
+  uint32_t hi = own ? (uint32_t)__double2hiint(v) : 0u;
+  if constexpr (S >= 2) { lo |= dpp<0xB1>(lo); hi |= dpp<0xB1>(hi); }
+  if constexpr (S >= 4) { lo |= dpp<0x4E>(lo); hi |= dpp<0x4E>(hi); }
+  if constexpr (S >= 8) { lo |= dpp<0x141>(lo); hi |= dpp<0x141>(hi); }
+  if constexpr (S >= 16) { lo |= dpp<0x140>(lo); hi |= dpp<0x140>(hi); }
+  if constexpr (S == 32) {
+    const uint32_t a = rl(lo, 0) | rl(lo, 16), b = rl(lo, 32) | rl(lo, 48);
+    const uint32_t c = rl(hi, 0) | rl(hi, 16), d = rl(hi, 32) | rl(hi, 48);
+    lo = lane < 32 ? a : b;
+    hi = lane < 32 ? c : d;
+  } else if constexpr (S >= 64) {
+    lo = (rl(lo, 0) | rl(lo, 16)) | (rl(lo, 32) | rl(lo, 48));
+    hi = (rl(hi, 0) | rl(hi, 16)) | (rl(hi, 32) | rl(hi, 48));
+  }
+  return __hiloint2double((int)hi, (int)lo);
+}
+
+// Lowest lane (relative to the segment, or to the wave for S >= 64) of each
+// segment where `pred` holds; -1 where it holds nowhere.
+template <int S>
+__device__ __forceinline__ int32_t seg_first(bool pred, int lane) {
+  const uint64_t b = __ballot(pred);
+  if constexpr (S >= 64) {
+    return __ffsll((unsigned long long)b) - 1;
+  } else {
+    const uint32_t half = lane < 32 ? (uint32_t)b : (uint32_t)(b >> 32);
+    const int sh = (lane & 31) & ~(S - 1);
+    const uint32_t mask = (S == 32) ? 0xffffffffu : ((1u << (S & 31)) - 1u);
+    return __ffs((half >> sh) & mask) - 1;
+  }
+}
+
+}  // namespace rt

@@ -24,6 +24,9 @@ struct DevPoint {
 
 enum : uint32_t { kFlagRejected = 1u, kFlagBadTrace = 2u, kFlagTimeRange = 4u };
 
+// rt_policy values as the kernels read them from DevPoint::policy.
+enum : int32_t { kPolicyLearned = 0, kPolicyRoundRobin = 1, kPolicyLeastLoaded = 2 };
+
 // Arguments of the replica-simulation kernels.
 struct SimArgs {
   const DevPoint* points;
@@ -40,26 +43,52 @@ struct SimArgs {
   int32_t* i_dec;
   int64_t* ttft;
   int64_t* span;
-  // Successor records of the per-instance FIFOs (one slot per request and
-  // pool, indexed by the global request index of the predecessor).
-  int4* sp;       // prefill: {release (double bits lo, hi), successor index, prompt tokens}
-  double* sd_t;   // decode release time
-  int4* sd_m;     // decode: {successor index, cache tokens p+o, ledger tokens o^, 0}
-  char* dummy;    // kDummyLanes private 64-byte slots (writes with nothing to write)
+  // Successor records of the per-instance FIFOs: kRecStride bytes per
+  // request, indexed by the global request index of the predecessor (see
+  // the offsets below).
+  char* rec;
+  char* dummy;  // kDummyLanes / 64 wave-private 64-byte slots (memory ops with nothing to do)
   uint32_t* flag;
 };
 
+// Layout of one request's scratch region.  For each pool, a pair of entries
+// {release time (double), index, cache tokens} describing the request's
+// first and second successor in the same instance's FIFO, and a pair of the
+// same successors' ledger tokens.  Kernels that keep one successor use the
+// first entry of each pair only.
+constexpr int kRecStride = 80;
+constexpr int kRecPairPre = 0;   // 2 x 16 bytes
+constexpr int kRecPairDec = 32;  // 2 x 16 bytes
+constexpr int kRecTokPre = 64;   // 2 x 4 bytes
+constexpr int kRecTokDec = 72;   // 2 x 4 bytes
+
 constexpr int kDummyLanes = 1 << 16;
 
-// Kernel classes: lanes per replica S (a power of two; S > 64 spans S/64
-// waves of one workgroup) and instances per lane for each pool.
+// Kernel classes.  kSeg: one replica per aligned segment of S <= 64 lanes of
+// one wave, prefill instances on the first lanes and decode instances on the
+// next, MP = MD instances per lane; `mode` fixes the scoring path (clock
+// backlog, ledger backlog, or a baseline policy).  kWide: S > 64 lanes (S/64
+// waves of one workgroup) hold MP prefill and MD decode instances each, any
+// mode.
+enum SimKind { kSeg = 0, kWide = 1 };
+enum SimMode { kModeTrue = 0, kModeProxy = 1, kModeBase = 2, kModeAny = 3 };
+
 struct SimClass {
-  int S, MP, MD;
+  int kind, S, MP, MD, mode;
 };
 
+// Every kernel class, segment classes first (in order of preference), and
+// the launch of one class over a work list.
 hipError_t launch_sim(const SimClass& c, const SimArgs& a, hipStream_t stream);
 int sim_class_count();
 SimClass sim_class(int i);
+// the two families behind them
+int seg_class_count();
+SimClass seg_class(int i);
+hipError_t launch_seg_class(const SimClass& c, const SimArgs& a, hipStream_t stream);
+int wide_class_count();
+SimClass wide_class(int i);
+hipError_t launch_wide_class(const SimClass& c, const SimArgs& a, hipStream_t stream);
 
 struct ScoreArgs {
   float w_b, w_s, w_q, rho, tau, inv_cap;

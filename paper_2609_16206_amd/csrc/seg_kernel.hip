@@ -1,0 +1,489 @@
+// Replica-batched simulation of the learned prefill/decode router for pools
+// that fit one wave, on gfx950.
+//
+// Method: Algorithm 1 per admission (score every instance of both pools with
+// the Section III-A cost equation, take each pool's argmin, prefill, transfer
+// the KV cache, decode, record), on the serial-service simulator of Section
+// III-D / Section VI.
+//
+// Mapping.  A replica is a chain of admissions; replicas are independent.
+// One replica occupies an aligned segment of S lanes of one wave (64 / S
+// replicas per wave).  Lanes [0, LP) hold the prefill instances and lanes
+// [LP, LP + LD) the decode instances, M per lane in blocked order (instance
+// j of a pool sits in that pool's lane j / M, slot j % M), so every lane
+// scores a single pool and the lowest lane holding a pool's minimum also
+// holds its lowest index.  Per-instance state (busy-until, queue, cache
+// occupancy, ledger tokens, the first three requests of its FIFO) lives in
+// registers; the per-request terms are computed by every lane of the
+// segment.  The two argmins are DPP reductions within 16-lane rows plus
+// readlane across rows.
+//
+// Issue model.  One wave per SIMD issues one instruction every ~4 cycles; a
+// lane mask written by a vector compare and read by the scalar unit, and a
+// taken branch, each cost several issue slots more.  The step is therefore
+// written so that every condition is a single vector compare feeding vector
+// selects (sentinels fold the conditions: a FIFO position beyond the FIFO's
+// length has release time +inf, and a rejected request uses now = -1, so
+// "the head has finished" is the one compare head <= now), and every memory
+// instruction is issued unconditionally (a lane with nothing to load or store
+// addresses its wave's dummy slot).  The only branches of a step are the
+// loop and a rare slow path.
+//
+// FIFO of in-flight requests per instance.  Service is in admission order,
+// so an instance releases its requests in admission order.  The first three
+// requests of each FIFO are kept in registers; the rest is a list in HBM
+// scratch in which every request's region holds its first and second
+// successor (release time, index, cache tokens; ledger tokens beside them),
+// written when those successors are admitted.  Up to two releases per
+// instance between two arrivals shift the register window, and the new
+// head's two successors are then loaded with one independent access (no
+// chain of dependent loads), merged at the end of the step; a third release
+// in one step takes the slow path, which waits.
+//
+// Memory ordering within a step (one wave): on gfx9 loads and stores share
+// one counter, so a wait for a load also waits for every older store.  The
+// step issues its loads (the next request, the successor pairs) before its
+// one wait, which it places after the arithmetic and before its own stores.
+// An instance's records are written and read by the one lane that owns it,
+// in program order, so a record is visible to every later load of it.
+//
+// Arithmetic of the cost: evaluated exactly as the equation is written, left
+// to right in float32, one rounding per operation (built with
+// -ffp-contract=off).  Times and token totals are integers held in doubles
+// (exact below 2^53; simulated times are kept below 2^52).
+#include "lane_ops.h"
+#include "rt_internal.h"
+
+namespace rt {
+namespace {
+
+constexpr double kInf = __builtin_huge_val();
+
+// One FIFO position: release time, request index, cache tokens, ledger tokens.
+struct Elem {
+  double t;
+  int32_t idx, fp, pt;
+};
+
+// A stored entry as it lies in scratch (16 bytes; ledger tokens apart).
+struct alignas(16) Entry {
+  double t;
+  int32_t idx, fp;
+};
+
+struct alignas(16) EntryPair {
+  Entry a, b;
+};
+
+struct Slot {
+  double busy;      // end of everything admitted so far
+  double kv;        // cache tokens in flight
+  double pend;      // ledger tokens in flight
+  int32_t q;        // requests in flight
+  int32_t tail;     // last admitted request
+  int32_t tail2;    // the one admitted before it
+  Elem h, n, n2;    // FIFO positions 0, 1, 2 (t = +inf beyond the FIFO)
+  Elem l1, l2;      // successors of the head, loaded this step
+  int32_t lq;       // FIFO length the loaded pair describes (0: nothing loaded)
+};
+
+__device__ __forceinline__ Elem none() { return Elem{kInf, 0, 0, 0}; }
+
+__device__ __forceinline__ void init_slot(Slot& s) {
+  s.busy = s.kv = s.pend = 0.0;
+  s.q = 0;
+  s.tail = s.tail2 = -1;
+  s.h = s.n = s.n2 = none();
+  s.l1 = s.l2 = Elem{0.0, 0, 0, 0};
+  s.lq = 0;
+}
+
+__device__ __forceinline__ Elem sel(bool c, const Elem& x, const Elem& y) {
+  return Elem{c ? x.t : y.t, c ? x.idx : y.idx, c ? x.fp : y.fp, c ? x.pt : y.pt};
+}
+
+// The loaded successors fill positions 1 and 2 where the FIFO (as it was
+// when they were loaded) reaches them.
+__device__ __forceinline__ void merge_pending(Slot& s) {
+  const bool m1 = s.lq >= 2, m2 = s.lq >= 3;
+  s.n = sel(m1, s.l1, s.n);
+  s.n2 = sel(m2, s.l2, s.n2);
+  s.lq = 0;
+}
+
+// Materializes the merged positions here, ahead of every later memory
+// instruction (an empty volatile asm that reads the registers and clobbers
+// memory), so that the wait for their load is not pushed past the stores.
+__device__ __forceinline__ void pin_window(const Slot& s) {
+  asm volatile("" ::"v"(s.n.t), "v"(s.n.idx), "v"(s.n.fp), "v"(s.n.pt), "v"(s.n2.t), "v"(s.n2.idx), "v"(s.n2.fp),
+               "v"(s.n2.pt)
+               : "memory");
+}
+
+template <bool kTok>
+__device__ __forceinline__ void load_pair(Slot& s, const char* rp, const char* tp) {
+  const EntryPair e = *reinterpret_cast<const EntryPair*>(rp);
+  s.l1 = Elem{e.a.t, e.a.idx, e.a.fp, e.a.fp};
+  s.l2 = Elem{e.b.t, e.b.idx, e.b.fp, e.b.fp};
+  if constexpr (kTok) {
+    const int2 k = *reinterpret_cast<const int2*>(tp);
+    s.l1.pt = k.x;
+    s.l2.pt = k.y;
+  }
+}
+
+template <int S, int M, int kMode, int kWaves>
+__global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
+  constexpr bool kTok = kMode == kModeProxy;  // the ledger is priced
+  constexpr bool kKv = kMode != kModeBase;    // occupancy is priced
+  constexpr int kSegs = 64 / S;               // replicas per wave
+  const int lane = threadIdx.x & 63;
+  const int sl = lane & (S - 1);
+  const int segw = (int)(threadIdx.x >> 6) * kSegs + lane / S;  // segment within the block
+  const int64_t item = (int64_t)blockIdx.x * (kWaves * kSegs) + segw;
+  const bool live = item < a.n_work;
+  const int rep = live ? a.work[item] : 0;
+  const int64_t base = live ? a.offsets[rep] : 0;
+  const int32_t R = live ? (int32_t)(a.offsets[rep + 1] - base) : 0;
+  const int pid = (live && a.param_point) ? a.param_point[rep] : 0;
+  const DevPoint& pt = a.points[pid];
+  const int32_t P = pt.P, D = pt.D, ncls = pt.n_classes, policy = pt.policy;
+  const int32_t LP = (P + M - 1) / M;  // lanes holding prefill instances
+  const bool isp = sl < LP;
+  const int32_t j0 = (isp ? sl : sl - LP) * M;  // this lane's first instance in its pool
+  const int32_t npool = isp ? P : D;
+  const float w_b = pt.w_b, w_s = pt.w_s, w_q = pt.w_q, rho = pt.rho;
+  const float inv = isp ? pt.inv_cap_pre : pt.inv_cap_dec;
+  const float tau = isp ? pt.tau_pre : pt.tau_dec;
+  const float basec = isp ? pt.pre_base : 0.0f;  // proxy ledger: base per in-flight prefill
+  const double pre_base_ns = (double)pt.pre_base_ns, pre_tok_ns = (double)pt.pre_tok_ns;
+  const double dec_tok_ns = (double)pt.dec_tok_ns, xfer_tok_ns = (double)pt.xfer_tok_ns;
+  char* const recb = a.rec + (isp ? kRecPairPre : kRecPairDec);
+  char* const tokb = a.rec + (isp ? kRecTokPre : kRecTokDec);
+  // The wave's dummy record: a negative request index whose region lies in
+  // the dummy area just before the records (record loads and stores with
+  // nothing to do use it, so that only an index is selected); and the wave's
+  // 64-byte dummy slot for output stores with nothing to write.
+  const uint32_t wave_id = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) & (kDummyLanes / 64 - 1);
+  const int64_t dmy = -1 - (int64_t)wave_id;
+  char* const dummy = a.dummy + (size_t)wave_id * 64;
+
+  // sigma per class of each segment's point, read a step ahead of its use
+  __shared__ float sig[kWaves * kSegs * kMaxClasses];
+  for (int k = sl; k < kMaxClasses; k += S) sig[segw * kMaxClasses + k] = pt.sigma[k];
+  __syncthreads();
+
+  Slot s[M];
+  bool ok[M];  // the slot holds an instance of the lane's pool
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    init_slot(s[m]);
+    ok[m] = live && j0 + m < npool;
+  }
+
+  // steps of this wave (wave-uniform, so the loop test is scalar)
+  const int32_t Rmax = __builtin_amdgcn_readfirstlane(wave_max_nonneg(R));
+
+  // The features of request t+1 are loaded during step t-1 (index clamped
+  // into the replica; request 0 of the trace for a segment without a
+  // replica), its class a step earlier still.
+  const int64_t rd_base = R > 0 ? base : 0;
+  const int32_t rd_last = R > 0 ? R - 1 : 0;
+  double last_now = 0.0;  // latest accepted arrival (arrivals must not decrease)
+
+  // Request validity: lengths >= 1, token sums within int32, class in range,
+  // the step belongs to the replica, arrival >= 0 and not before the last
+  // accepted one.  A rejected request is not routed and changes no state; it
+  // releases nothing (now = -1).
+  struct Req {
+    double now, now_eff;
+    int32_t p, o, oh, po, poh;
+    bool go;
+  };
+  auto admit_check = [&](int32_t t, int64_t arr, int32_t p, int32_t o, int32_t oh, uint32_t c) {
+    Req q;
+    q.p = p;
+    q.o = o;
+    q.oh = oh;
+    q.po = (int32_t)((uint32_t)p + (uint32_t)o);
+    q.poh = (int32_t)((uint32_t)p + (uint32_t)oh);
+    const int32_t vm = min(min(min(p, o), min(oh, q.po)), min(min(q.poh, ncls - (int32_t)c), R - t));
+    q.now = i64_to_f64(arr);
+    const double xv = opaque(vm) >= 1 ? q.now : -1.0;
+    q.go = xv >= last_now;
+    q.now_eff = q.go ? xv : -1.0;
+    last_now = __builtin_fmax(last_now, xv);
+    return q;
+  };
+
+  // Release: up to two completions per instance from the register window;
+  // the new head's successors are loaded unconditionally (merged one step
+  // later).
+  auto release_fast = [&](double now_eff) {
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      Slot& x = s[m];
+      const bool p1 = x.h.t <= now_eff;
+      const bool p2 = x.n.t <= now_eff;  // implies p1 (release times do not decrease)
+      x.q -= (p1 ? 1 : 0) + (p2 ? 1 : 0);
+      if constexpr (kKv) x.kv = x.kv - ((p1 ? (double)x.h.fp : 0.0) + (p2 ? (double)x.n.fp : 0.0));
+      if constexpr (kTok) x.pend = x.pend - ((p1 ? (double)x.h.pt : 0.0) + (p2 ? (double)x.n.pt : 0.0));
+      const Elem h1 = sel(p2, x.n2, sel(p1, x.n, x.h));
+      Elem n1 = sel(p1, x.n2, x.n);
+      n1.t = p2 ? kInf : n1.t;
+      x.h = h1;
+      x.n = n1;
+      x.n2.t = p1 ? kInf : x.n2.t;
+      const int32_t lq = opaque(p1 ? x.q : 0);
+      const bool ld = lq >= 2;
+      const int64_t g = ld ? base + min(max(x.h.idx, 0), max(R - 1, 0)) : dmy;
+      load_pair<kTok>(x, recb + g * kRecStride, tokb + g * kRecStride);
+      x.lq = lq;
+    }
+  };
+  // More completions than the window holds (rare): wait for the loaded
+  // successors and release again, until no head has finished.
+  auto release = [&](double now_eff) {
+    release_fast(now_eff);
+    double hmin = s[0].h.t;
+#pragma unroll
+    for (int m = 1; m < M; ++m) hmin = __builtin_fmin(hmin, s[m].h.t);
+    if (__builtin_expect(__any(hmin <= now_eff), 0)) {
+      do {
+#pragma unroll
+        for (int m = 0; m < M; ++m) merge_pending(s[m]);
+        release_fast(now_eff);
+        hmin = s[0].h.t;
+#pragma unroll
+        for (int m = 1; m < M; ++m) hmin = __builtin_fmin(hmin, s[m].h.t);
+      } while (__any(hmin <= now_eff));
+    }
+  };
+
+  // Raw features of one request as loaded.
+  struct Feat {
+    int64_t arr;
+    int32_t p, o, oh;
+    uint32_t c;
+  };
+  auto load_feat = [&](Feat& f, int32_t tt) {
+    const int64_t g = rd_base + min(tt, rd_last);
+    f.arr = a.arrival[g];
+    f.p = a.plen[g];
+    f.o = a.olen[g];
+    f.oh = a.ohat[g];
+    f.c = a.cls[g];
+  };
+
+  int32_t rr = 0;     // round robin: t mod (size of this lane's pool)
+  double tmax = 0.0;  // latest decode end this lane recorded (time-range check)
+  uint32_t rej = 0;   // a rejected request was recorded by this lane
+  Req cur;            // request t, checked, its releases done
+  float sg;           // sigma of request t's class
+
+  // Step t: score, argmin, serve and record request t; store; then merge the
+  // successors loaded during the releases for request t (a step ago), check
+  // request t+1 (features `nx`, loaded a step ago) and do its releases, and
+  // load the features of request t+2 into `ld`.
+  auto step = [&](int32_t t, Feat& nx, Feat& ld) {
+    const int32_t p = cur.p, o = cur.o, oh = cur.oh, po = cur.po, poh = cur.poh;
+    const double now = cur.now;
+    const bool go = cur.go;
+
+    // 1. score this lane's instances
+    const int32_t cnt = isp ? p : oh;           // priced tokens of the pool
+    const float work = w_s * (float)cnt * tau;  // w_s * p * tau_pre, or w_s * o^ * tau_dec
+    const double need = (double)(isp ? p : poh);
+    uint32_t bkey = 0xffffffffu;
+    int32_t bm = 0;
+    double bbusy = s[0].busy;
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      const Slot& x = s[m];
+      uint32_t key;
+      if constexpr (kMode == kModeBase) {
+        key = policy == kPolicyLeastLoaded ? (uint32_t)x.q : ((j0 + m) == rr ? 0u : 1u);
+      } else {
+        float bl;
+        if constexpr (kMode == kModeTrue)
+          bl = (float)__builtin_fmax(x.busy - now, 0.0) * 1e-9f;
+        else
+          bl = tau * (float)x.pend + basec * (float)x.q;
+        const float press = (float)(x.kv + need) * inv;
+        const float load = w_b * bl * sg;
+        const float size = work * (1.0f + rho * press) * sg;
+        const float cost = load + size + w_q * (float)x.q;
+        key = cost != cost ? 0x7fc00000u : __float_as_uint(cost);
+      }
+      key = ok[m] ? key : 0xffffffffu;
+      if (m == 0) {
+        bkey = key;
+      } else {
+        const bool b = key < bkey;
+        bkey = b ? key : bkey;
+        bm = b ? m : bm;
+        bbusy = b ? x.busy : bbusy;
+      }
+    }
+
+    // 2. argmin of each pool over the segment, lowest index on equal keys
+    uint32_t kp = isp ? bkey : 0xffffffffu, kd = isp ? 0xffffffffu : bkey;
+    const uint32_t kp0 = kp, kd0 = kd;
+    seg_min2<S>(kp, kd, lane);
+    const int32_t wp = seg_first<S>(kp0 == kp, lane);  // winning lanes
+    const int32_t wd = seg_first<S>(kd0 == kd, lane);
+    int32_t mp = 0, md = 0;  // winning slots
+    if constexpr (M > 1) {
+      mp = (int32_t)seg_or<S>(sl == wp ? (uint32_t)bm : 0u, lane);
+      md = (int32_t)seg_or<S>(sl == wd ? (uint32_t)bm : 0u, lane);
+    }
+    const int32_t ip = wp * M + mp;
+    const int32_t id = (wd - LP) * M + md;
+
+    // 3. serve: prefill, KV transfer, decode (exact integers in doubles)
+    const double s_pre = __builtin_fma((double)p, pre_tok_ns, pre_base_ns);
+    const double pf_end = seg_bcast_f64<S>(__builtin_fmax(now, bbusy) + s_pre, sl == wp, lane);
+    const double kv_at = pf_end + (double)p * xfer_tok_ns;
+    const double de = __builtin_fmax(kv_at, bbusy) + (double)(o - 1) * dec_tok_ns;  // on the decode winner
+    const double end = isp ? pf_end : de;
+    const int32_t fp = isp ? p : po;  // cache tokens held until release
+    const int32_t tk = isp ? p : oh;  // ledger tokens
+    const Elem z{end, t, fp, tk};
+    const int32_t wl = go ? (isp ? wp : wd) : -1;
+    const bool own_lane = opaque(wl) == sl;
+    const int32_t wm = own_lane ? (isp ? mp : md) : -1;
+    int32_t st1 = -1, st2 = -1;  // requests whose first / second successor is z
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      Slot& x = s[m];
+      const bool own = (M == 1) ? own_lane : (opaque(wm) == m);
+      const int32_t w = opaque(own ? x.q : -1);  // z's FIFO position
+      x.h = sel(w == 0, z, x.h);
+      x.n = sel(w == 1, z, x.n);
+      x.n2 = sel(w == 2, z, x.n2);
+      st1 = w >= 1 ? x.tail : st1;
+      st2 = w >= 2 ? x.tail2 : st2;
+      x.tail2 = own ? x.tail : x.tail2;
+      x.tail = own ? t : x.tail;
+      x.q = own ? x.q + 1 : x.q;
+      if constexpr (kKv) x.kv = x.kv + (own ? (double)fp : 0.0);
+      if constexpr (kTok) x.pend = x.pend + (own ? (double)tk : 0.0);
+      x.busy = own ? end : x.busy;
+    }
+
+    // 4. the outcome, written by the decode winner (lane 0 of the segment for
+    // a rejected request); the records of z; every lane stores (the ones
+    // with nothing to store address the dummies)
+    {
+      const int32_t ow = opaque((R - t) >= 1 ? (go ? wd : 0) : -1);
+      const bool own_out = ow == sl;
+      const int32_t o_ip = go ? ip : -1, o_id = go ? id : -1;
+      const int64_t o_ttft = go ? f64_to_i64(pf_end - now) : -1;
+      const int64_t o_span = go ? f64_to_i64(de - pf_end) : -1;
+      tmax = __builtin_fmax(tmax, opaque(opaque(go ? wd : -1) == sl ? de : 0.0));
+      rej |= opaque(go ? 0u : 1u) & opaque(own_out ? 1u : 0u);
+      const Entry ze{end, t, fp};
+      const bool s1 = opaque(st1) >= 0, s2 = opaque(st2) >= 0;
+      const int64_t g1 = s1 ? base + st1 : dmy, g2 = s2 ? base + st2 : dmy;
+      *reinterpret_cast<Entry*>(recb + g1 * kRecStride) = ze;
+      *reinterpret_cast<Entry*>(recb + g2 * kRecStride + 16) = ze;
+      if constexpr (kTok) {
+        *reinterpret_cast<int32_t*>(tokb + g1 * kRecStride) = tk;
+        *reinterpret_cast<int32_t*>(tokb + g2 * kRecStride + 4) = tk;
+      }
+      const int64_t go_i = base + t;
+      int32_t* const d_ip = own_out ? a.i_pre + go_i : reinterpret_cast<int32_t*>(dummy);
+      int32_t* const d_id = own_out ? a.i_dec + go_i : reinterpret_cast<int32_t*>(dummy + 4);
+      int64_t* const d_tt = own_out ? a.ttft + go_i : reinterpret_cast<int64_t*>(dummy + 8);
+      int64_t* const d_sp = own_out ? a.span + go_i : reinterpret_cast<int64_t*>(dummy + 16);
+      *d_ip = o_ip;
+      *d_id = o_id;
+      *d_tt = o_ttft;
+      *d_sp = o_span;
+    }
+    if constexpr (kMode == kModeBase) rr = (rr + 1 == npool) ? 0 : rr + 1;
+
+    // 5. the successors loaded during request t's releases (the step's one
+    // wait: those loads and the features of request t+1 were issued a step
+    // ago), kept apart from the surrounding code by the scheduling barriers
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      merge_pending(s[m]);
+      pin_window(s[m]);
+    }
+    asm volatile("" : "+v"(nx.arr), "+v"(nx.p), "+v"(nx.o), "+v"(nx.oh), "+v"(nx.c));
+    __builtin_amdgcn_sched_barrier(0);
+
+    // 6. request t+1: check, sigma, releases; load request t+2
+    cur = admit_check(t + 1, nx.arr, nx.p, nx.o, nx.oh, nx.c);
+    sg = sig[segw * kMaxClasses + (nx.c & (kMaxClasses - 1))];
+    release(cur.now_eff);
+    load_feat(ld, t + 2);
+  };
+
+  // request 0 (nothing to release yet); requests 1 and 2 in flight
+  Feat fa, fb;
+  load_feat(fa, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  cur = admit_check(0, fa.arr, fa.p, fa.o, fa.oh, fa.c);
+  sg = sig[segw * kMaxClasses + (fa.c & (kMaxClasses - 1))];
+  load_feat(fa, 1);
+  // enter the loop with nothing in flight, so that the loop header needs no
+  // wait
+  __builtin_amdgcn_s_waitcnt(0);
+
+  // two steps per iteration, so that the features loaded in one step are
+  // read in the next from the same registers
+  for (int32_t t = 0; __builtin_amdgcn_readfirstlane(t) < Rmax; t += 2) {
+    step(t, fa, fb);
+    if (__builtin_amdgcn_readfirstlane(t) + 1 < Rmax) step(t + 1, fb, fa);
+  }
+  const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u);
+  if (flag) atomicOr(a.flag, flag);
+}
+
+// Four waves per workgroup (one per SIMD of a compute unit).
+constexpr int kSegWaves = 4;
+
+template <int S, int M, int kMode>
+hipError_t launch_seg(const SimArgs& a, hipStream_t stream) {
+  if (a.n_work <= 0) return hipSuccess;
+  const int64_t per_block = kSegWaves * (64 / S);
+  const int64_t blocks = (a.n_work + per_block - 1) / per_block;
+  hipLaunchKernelGGL((seg_kernel<S, M, kMode, kSegWaves>), dim3((unsigned)blocks), dim3(64 * kSegWaves), 0, stream,
+                     a);
+  return hipGetLastError();
+}
+
+struct SegEntry {
+  int S, M, mode;
+  hipError_t (*fn)(const SimArgs&, hipStream_t);
+};
+
+#define RT_SEG3(S, M)                                                                                \
+  {S, M, kModeTrue, launch_seg<S, M, kModeTrue>}, {S, M, kModeProxy, launch_seg<S, M, kModeProxy>}, \
+      {S, M, kModeBase, launch_seg<S, M, kModeBase>}
+
+// In order of preference: the fewest instances per lane, then the narrowest
+// segment that holds both pools.
+const SegEntry kSegTable[] = {RT_SEG3(2, 1),  RT_SEG3(4, 1),  RT_SEG3(8, 1),  RT_SEG3(16, 1),
+                              RT_SEG3(32, 1), RT_SEG3(64, 1), RT_SEG3(64, 2), RT_SEG3(64, 4)};
+#undef RT_SEG3
+
+}  // namespace
+
+int seg_class_count() { return (int)(sizeof(kSegTable) / sizeof(kSegTable[0])); }
+
+SimClass seg_class(int i) {
+  const SegEntry& e = kSegTable[i];
+  return SimClass{kSeg, e.S, e.M, e.M, e.mode};
+}
+
+hipError_t launch_seg_class(const SimClass& c, const SimArgs& a, hipStream_t stream) {
+  for (const SegEntry& e : kSegTable)
+    if (e.S == c.S && e.M == c.MP && e.mode == c.mode) return e.fn(a, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace rt

@@ -1,4 +1,6 @@
-// Replica-batched simulation of the learned prefill/decode router on gfx950.
+// Replica-batched simulation of the learned prefill/decode router on gfx950,
+// for pools wider than one wave segment holds (the general kernel; narrower
+// pools run the segment kernels).
 //
 // Method: Algorithm 1 per admission (score both pools with the Section III-A
 // cost equation, take each argmin, prefill, transfer KV, decode, record),
@@ -22,8 +24,8 @@
 // double-to-float conversion rounds the exact integer to nearest even, the
 // same float as an int64-to-float conversion.  On gfx950 these are single
 // full-rate f64 instructions, where int64 arithmetic takes 2-3 instructions
-// and an int64-to-float conversion a long sequence.  Times at or beyond 2^53
-// ns (104 days) set a flag bit.
+// and an int64-to-float conversion a long sequence.  Times at or beyond 2^52
+// ns (52 days) set a flag bit.
 //
 // FIFO of in-flight requests per instance.  Service is in admission order,
 // so each instance releases its requests in admission order and only the
@@ -54,25 +56,11 @@
 // Arithmetic of the cost: evaluated exactly as the equation is written, left
 // to right in float32, one rounding per operation (built with
 // -ffp-contract=off).
+#include "lane_ops.h"
 #include "rt_internal.h"
 
 namespace rt {
 namespace {
-
-constexpr double kTwo32 = 4294967296.0;
-constexpr double kTimeLimit = 9007199254740992.0;  // 2^53
-
-// int64 -> double, exact for |x| < 2^53.
-__device__ __forceinline__ double i64_to_f64(int64_t x) {
-  return __builtin_fma((double)(int32_t)(x >> 32), kTwo32, (double)(uint32_t)(uint64_t)x);
-}
-
-// double holding an integer in [0, 2^53) -> int64.
-__device__ __forceinline__ int64_t f64_to_i64(double x) {
-  const double hi = __builtin_trunc(x * (1.0 / kTwo32));
-  const double lo = __builtin_fma(-hi, kTwo32, x);
-  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
-}
 
 // Per-instance state.  Plain scalars only, copied field by field with value
 // selects, so that everything stays in registers.
@@ -132,9 +120,15 @@ __device__ __forceinline__ int64_t slot_of(int64_t base, int32_t idx, int32_t R)
   return base + idx;
 }
 
-// Records: prefill {release (double bits), successor index, prompt tokens}
-// in one 16-byte unit; decode {release} in 8 bytes plus {successor index,
-// cache tokens p+o, ledger tokens o^, 0} in 16.
+// Records: {release (double bits), successor index, cache tokens} in the
+// first entry of the request's pair for the pool; the ledger tokens of a
+// decode record in the first entry of its token pair (a prefill record's
+// ledger tokens are its cache tokens, the prompt).
+template <typename T>
+__device__ __forceinline__ T* rec_at(const SimArgs& a, int64_t g, int off) {
+  return reinterpret_cast<T*>(a.rec + g * kRecStride + off);
+}
+
 __device__ __forceinline__ void read_pre(const int4& m, double& t, int32_t& idx, int32_t& fp, int32_t& pt) {
   t = __hiloint2double(m.y, m.x);
   idx = m.z;
@@ -158,15 +152,15 @@ __device__ __forceinline__ void pop_fast(Inst& s, bool pp, const SimArgs& a, con
   const bool ld = pp && s.q >= 2;
   const int64_t g = slot_of(base, s.h_idx, R);
   if constexpr (kDec) {
-    const double* pt = ld ? a.sd_t + g : reinterpret_cast<const double*>(dummy);
-    const int4* pm = ld ? a.sd_m + g : reinterpret_cast<const int4*>(dummy + 16);
-    s.l_t = *pt;
+    const int4* pm = ld ? rec_at<int4>(a, g, kRecPairDec) : reinterpret_cast<const int4*>(dummy);
+    const int32_t* pq = ld ? rec_at<int32_t>(a, g, kRecTokDec) : reinterpret_cast<const int32_t*>(dummy + 16);
     const int4 m = *pm;
-    s.l_idx = m.x;
-    s.l_fp = m.y;
-    s.l_pt = m.z;
+    s.l_t = __hiloint2double(m.y, m.x);
+    s.l_idx = m.z;
+    s.l_fp = m.w;
+    s.l_pt = *pq;
   } else {
-    const int4* pm = ld ? a.sp + g : reinterpret_cast<const int4*>(dummy);
+    const int4* pm = ld ? rec_at<int4>(a, g, kRecPairPre) : reinterpret_cast<const int4*>(dummy);
     read_pre(*pm, s.l_t, s.l_idx, s.l_fp, s.l_pt);
   }
   s.lp = ld ? 1 : 0;
@@ -187,13 +181,13 @@ __device__ __forceinline__ void pop_slow(Inst& s, const SimArgs& a, int64_t base
   if (s.q >= 2) {
     const int64_t g = slot_of(base, s.h_idx, R);
     if constexpr (kDec) {
-      s.n_t = a.sd_t[g];
-      const int4 m = a.sd_m[g];
-      s.n_idx = m.x;
-      s.n_fp = m.y;
-      s.n_pt = m.z;
+      const int4 m = *rec_at<int4>(a, g, kRecPairDec);
+      s.n_t = __hiloint2double(m.y, m.x);
+      s.n_idx = m.z;
+      s.n_fp = m.w;
+      s.n_pt = *rec_at<int32_t>(a, g, kRecTokDec);
     } else {
-      read_pre(a.sp[g], s.n_t, s.n_idx, s.n_fp, s.n_pt);
+      read_pre(*rec_at<int4>(a, g, kRecPairPre), s.n_t, s.n_idx, s.n_fp, s.n_pt);
     }
   }
 }
@@ -227,87 +221,6 @@ __device__ __forceinline__ float cost_eq(float w_b, float rho, float w_q, float 
   const float load = w_b * backlog_s * sg;
   const float size = work * (1.0f + rho * press) * sg;
   return load + size + w_q * (float)q;
-}
-
-// ---------------------------------------------------------------------------
-// Segment collectives over aligned groups of S lanes.  Within a 16-lane row:
-// quad_perm xor 1, xor 2, then half-row mirror and row mirror (each step
-// pairs every lane with one from the other half of its group, so after
-// log2(S) steps every lane holds the group result).  Across rows: readlane
-// of each row.  For S > 64 these reduce over the wave.
-// ---------------------------------------------------------------------------
-template <int C>
-__device__ __forceinline__ uint32_t dpp(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, C, 0xF, 0xF, true);
-}
-
-__device__ __forceinline__ uint32_t rl(uint32_t v, int lane) {
-  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
-}
-
-template <int S>
-__device__ __forceinline__ uint32_t seg_min(uint32_t v, int lane) {
-  if constexpr (S >= 2) v = min(v, dpp<0xB1>(v));
-  if constexpr (S >= 4) v = min(v, dpp<0x4E>(v));
-  if constexpr (S >= 8) v = min(v, dpp<0x141>(v));
-  if constexpr (S >= 16) v = min(v, dpp<0x140>(v));
-  if constexpr (S == 32) {
-    const uint32_t a = min(rl(v, 0), rl(v, 16)), b = min(rl(v, 32), rl(v, 48));
-    v = lane < 32 ? a : b;
-  } else if constexpr (S >= 64) {
-    v = min(min(rl(v, 0), rl(v, 16)), min(rl(v, 32), rl(v, 48)));
-  }
-  return v;
-}
-
-template <int S>
-__device__ __forceinline__ uint32_t seg_or(uint32_t v, int lane) {
-  if constexpr (S >= 2) v |= dpp<0xB1>(v);
-  if constexpr (S >= 4) v |= dpp<0x4E>(v);
-  if constexpr (S >= 8) v |= dpp<0x141>(v);
-  if constexpr (S >= 16) v |= dpp<0x140>(v);
-  if constexpr (S == 32) {
-    const uint32_t a = rl(v, 0) | rl(v, 16), b = rl(v, 32) | rl(v, 48);
-    v = lane < 32 ? a : b;
-  } else if constexpr (S >= 64) {
-    v = (rl(v, 0) | rl(v, 16)) | (rl(v, 32) | rl(v, 48));
-  }
-  return v;
-}
-
-// Maximum over the whole wave of non-negative values.
-__device__ __forceinline__ int32_t wave_max_nonneg(int32_t v) {
-  uint32_t u = (uint32_t)v;
-  u = max(u, dpp<0xB1>(u));
-  u = max(u, dpp<0x4E>(u));
-  u = max(u, dpp<0x141>(u));
-  u = max(u, dpp<0x140>(u));
-  u = max(max(rl(u, 0), rl(u, 16)), max(rl(u, 32), rl(u, 48)));
-  return (int32_t)u;
-}
-
-// Broadcast a double from the one lane of each segment where `own` holds
-// (every other lane contributes 0 bits to an OR).
-template <int S>
-__device__ __forceinline__ double seg_bcast_f64(double v, bool own, int lane) {
-  const int lo = own ? __double2loint(v) : 0;
-  const int hi = own ? __double2hiint(v) : 0;
-  return __hiloint2double((int)seg_or<S>((uint32_t)hi, lane), (int)seg_or<S>((uint32_t)lo, lane));
-}
-
-// Lowest lane (relative to the segment, or to the wave for S >= 64) of each
-// segment where `pred` holds.
-template <int S>
-__device__ __forceinline__ int32_t seg_first(bool pred, int lane) {
-  const uint64_t b = __ballot(pred);
-  if constexpr (S >= 64) {
-    return __ffsll((unsigned long long)b) - 1;
-  } else {
-    const uint32_t half = lane < 32 ? (uint32_t)b : (uint32_t)(b >> 32);
-    const int sh = (lane & 31) & ~(S - 1);
-    const uint32_t mask = (S == 32) ? 0xffffffffu : ((1u << (S & 31)) - 1u);
-    return __ffs((half >> sh) & mask) - 1;
-  }
 }
 
 struct Partial {
@@ -530,7 +443,7 @@ __global__ void __launch_bounds__(S > 64 ? S : 256) sim_kernel(SimArgs a) {
     }
 
     // 3c. serve: prefill, KV transfer, decode, each FIFO in admission order
-    // (every product below is an exact integer under the 2^53 limit)
+    // (every product below is an exact integer below the time limit)
     const double s_pre = __builtin_fma((double)p, pre_tok_ns, pre_base_ns);
     const double s_dec = (double)(o - 1) * dec_tok_ns;
     const double xfer = (double)p * xfer_tok_ns;
@@ -602,10 +515,10 @@ __global__ void __launch_bounds__(S > 64 ? S : 256) sim_kernel(SimArgs a) {
       a.ttft[d_out] = d_ttft;
       a.span[d_out] = d_span;
     }
-    if (d_ps >= 0) a.sp[d_ps] = make_int4(__double2loint(d_pt), __double2hiint(d_pt), d_pidx, d_pp);
+    if (d_ps >= 0) *rec_at<int4>(a, d_ps, kRecPairPre) = make_int4(__double2loint(d_pt), __double2hiint(d_pt), d_pidx, d_pp);
     if (d_ds >= 0) {
-      a.sd_t[d_ds] = d_dt;
-      a.sd_m[d_ds] = make_int4(d_didx, d_dfp, d_dpt, 0);
+      *rec_at<int4>(a, d_ds, kRecPairDec) = make_int4(__double2loint(d_dt), __double2hiint(d_dt), d_didx, d_dfp);
+      *rec_at<int32_t>(a, d_ds, kRecTokDec) = d_dpt;
     }
     rr_pre = (rr_pre + 1 == P) ? 0 : rr_pre + 1;
     rr_dec = (rr_dec + 1 == D) ? 0 : rr_dec + 1;
@@ -630,30 +543,39 @@ hipError_t launch_one(const SimArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-struct ClassEntry {
-  SimClass c;
+struct WideEntry {
+  int S, MP, MD;
   hipError_t (*fn)(const SimArgs&, hipStream_t);
 };
 
-// Cheapest first: the host picks the first class that fits a point.
-const ClassEntry kClasses[] = {
-    {{1, 1, 1}, launch_one<1, 1, 1>},       {{2, 1, 1}, launch_one<2, 1, 1>},
-    {{4, 1, 1}, launch_one<4, 1, 1>},       {{8, 1, 1}, launch_one<8, 1, 1>},
-    {{16, 1, 1}, launch_one<16, 1, 1>},     {{32, 1, 1}, launch_one<32, 1, 1>},
-    {{64, 1, 1}, launch_one<64, 1, 1>},     {{64, 2, 2}, launch_one<64, 2, 2>},
-    {{256, 1, 4}, launch_one<256, 1, 4>},   {{512, 2, 2}, launch_one<512, 2, 2>},
+// Pools wider than one wave segment holds (the segment kernels take the
+// rest); the host picks the first class that fits a point.
+const WideEntry kWideTable[] = {
+    {256, 1, 4, launch_one<256, 1, 4>},
+    {512, 2, 2, launch_one<512, 2, 2>},
 };
 
 }  // namespace
 
-int sim_class_count() { return (int)(sizeof(kClasses) / sizeof(kClasses[0])); }
+int wide_class_count() { return (int)(sizeof(kWideTable) / sizeof(kWideTable[0])); }
 
-SimClass sim_class(int i) { return kClasses[i].c; }
+SimClass wide_class(int i) {
+  const WideEntry& e = kWideTable[i];
+  return SimClass{kWide, e.S, e.MP, e.MD, kModeAny};
+}
+
+hipError_t launch_wide_class(const SimClass& c, const SimArgs& a, hipStream_t stream) {
+  for (const WideEntry& e : kWideTable)
+    if (e.S == c.S && e.MP == c.MP && e.MD == c.MD) return e.fn(a, stream);
+  return hipErrorInvalidValue;
+}
+
+int sim_class_count() { return seg_class_count() + wide_class_count(); }
+
+SimClass sim_class(int i) { return i < seg_class_count() ? seg_class(i) : wide_class(i - seg_class_count()); }
 
 hipError_t launch_sim(const SimClass& c, const SimArgs& a, hipStream_t stream) {
-  for (const ClassEntry& e : kClasses)
-    if (e.c.S == c.S && e.c.MP == c.MP && e.c.MD == c.MD) return e.fn(a, stream);
-  return hipErrorInvalidValue;
+  return c.kind == kSeg ? launch_seg_class(c, a, stream) : launch_wide_class(c, a, stream);
 }
 
 }  // namespace rt

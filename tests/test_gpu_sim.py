@@ -43,7 +43,8 @@ def test_cluster_full_size():
 
 def _mixed_points():
     """Pool shapes that exercise every kernel class, with all policies/modes."""
-    shapes = [(1, 1), (2, 2), (3, 4), (2, 6), (5, 16), (2, 32), (33, 64), (70, 100), (128, 1024), (1000, 300)]
+    shapes = [(1, 1), (2, 2), (3, 4), (2, 6), (4, 9), (5, 16), (2, 32), (33, 64), (70, 100), (128, 1024),
+              (1000, 300), (2, 64), (60, 70), (1, 63), (64, 64)]
     pts = []
     for k, (P, D) in enumerate(shapes):
         pol = ("learned", "learned", "round_robin", "least_loaded")[k % 4]
