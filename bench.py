@@ -58,7 +58,9 @@ def _source_hash(files):
     return h.hexdigest()[:16]
 
 
-SIM_SOURCES = ["paper_2609_16206_amd/csrc/sim_kernel.hip", "paper_2609_16206_amd/csrc/rt_internal.h"]
+SIM_SOURCES = ["paper_2609_16206_amd/csrc/" + f for f in (
+    "seg_kernel.h", "seg_true.hip", "seg_proxy.hip", "seg_base.hip", "seg_classes.hip", "sim_kernel.hip",
+    "lane_ops.h", "rt_internal.h")]
 SCORE_SOURCES = ["paper_2609_16206_amd/csrc/score_kernel.hip", "paper_2609_16206_amd/csrc/rt_internal.h"]
 
 

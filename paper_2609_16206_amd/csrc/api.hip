@@ -42,6 +42,7 @@ struct DeviceScope {
 bool finite_nonneg(float x) { return std::isfinite(x) && x >= 0.0f; }
 
 constexpr int64_t kMaxNs = int64_t(1) << 40;
+constexpr int kSimds = 256 * 4;  // MI355X: 256 compute units x 4 SIMDs
 
 std::string check_point(const rt_point& p) {
   if (p.n_prefill < 1 || p.n_decode < 1) return "pool sizes must be >= 1";
@@ -106,23 +107,34 @@ int point_mode(const rt_point& p) {
   return p.backlog_mode == RT_BACKLOG_TRUE ? rt::kModeTrue : rt::kModeProxy;
 }
 
-// The first kernel class (classes are listed in order of preference) that
-// holds both pools of a point: a segment class of the point's mode whose S
-// lanes hold ceil(P / M) prefill lanes and ceil(D / M) decode lanes, else a
-// wide class.
-int pick_class(const rt_point& p) {
-  const int mode = point_mode(p);
-  for (int i = 0; i < rt::sim_class_count(); ++i) {
-    const rt::SimClass c = rt::sim_class(i);
-    if (c.kind == rt::kSeg) {
-      if (c.mode != mode) continue;
-      const int lanes = (p.n_prefill + c.MP - 1) / c.MP + (p.n_decode + c.MD - 1) / c.MD;
-      if (lanes <= c.S) return i;
-    } else if (p.n_prefill <= c.S * c.MP && p.n_decode <= c.S * c.MD) {
-      return i;
-    }
+// Does kernel class c hold both pools of point p?  A segment class of the
+// point's mode needs ceil(P / M) prefill lanes and ceil(D / M) decode lanes
+// within its S; a wide class holds P <= S * MP and D <= S * MD.
+bool class_fits(const rt::SimClass& c, const rt_point& p) {
+  if (c.kind == rt::kSeg) {
+    if (c.mode != point_mode(p)) return false;
+    const int lanes = (p.n_prefill + c.MP - 1) / c.MP + (p.n_decode + c.MD - 1) / c.MD;
+    return lanes <= c.S;
   }
-  return -1;
+  return p.n_prefill <= c.S * c.MP && p.n_decode <= c.S * c.MD;
+}
+
+// Every class that holds a point, in the order the classes are listed (the
+// first has the shortest step).
+std::vector<int> fitting_classes(const rt_point& p) {
+  std::vector<int> out;
+  for (int i = 0; i < rt::sim_class_count(); ++i)
+    if (class_fits(rt::sim_class(i), p)) out.push_back(i);
+  return out;
+}
+
+// Issue slots of one step of a segment class, roughly: the per-request work
+// every lane repeats, the per-instance work of each of M slots, and one DPP
+// level of the argmins per doubling of the segment.
+double seg_step_cost(const rt::SimClass& c) {
+  int lg = 0;
+  while ((1 << lg) < c.S) ++lg;
+  return 150.0 + 70.0 * c.MP + 10.0 * lg;
 }
 
 }  // namespace
@@ -130,7 +142,7 @@ int pick_class(const rt_point& p) {
 struct rt_sim {
   int device = 0;
   std::vector<rt_point> points;
-  std::vector<int> point_class;
+  std::vector<std::vector<int>> point_classes;  // fitting classes of each point
   rt::DevPoint* d_points = nullptr;
   uint32_t* d_flag = nullptr;
   char* d_scratch = nullptr;
@@ -176,7 +188,7 @@ rt_status rt_sim_create(const rt_point* points, int32_t n_points, int32_t device
   hipError_t e = hipGetDeviceCount(&n_dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDeviceCount");
   if (device < 0 || device >= n_dev) return fail(RT_EINVAL, "rt_sim_create: no such device");
-  std::vector<int> cls(n_points);
+  std::vector<std::vector<int>> cls(n_points);
   for (int32_t i = 0; i < n_points; ++i) {
     const std::string msg = check_point(points[i]);
     if (!msg.empty()) {
@@ -185,8 +197,9 @@ rt_status rt_sim_create(const rt_point* points, int32_t n_points, int32_t device
                               : RT_EINVAL;
       return fail(s, "rt_sim_create: point " + std::to_string(i) + ": " + msg);
     }
-    cls[i] = pick_class(points[i]);
-    if (cls[i] < 0) return fail(RT_EUNSUPPORTED, "rt_sim_create: point " + std::to_string(i) + ": no kernel for this pool shape");
+    cls[i] = fitting_classes(points[i]);
+    if (cls[i].empty())
+      return fail(RT_EUNSUPPORTED, "rt_sim_create: point " + std::to_string(i) + ": no kernel for this pool shape");
   }
   DeviceScope ds(device);
   if (ds.err != hipSuccess) return hip_fail(ds.err, "hipSetDevice");
@@ -194,7 +207,7 @@ rt_status rt_sim_create(const rt_point* points, int32_t n_points, int32_t device
   if (!s) return fail(RT_ENOMEM, "rt_sim_create: host allocation");
   s->device = device;
   s->points.assign(points, points + n_points);
-  s->point_class = cls;
+  s->point_classes = cls;
   std::vector<rt::DevPoint> dev(n_points);
   for (int32_t i = 0; i < n_points; ++i) dev[i] = to_dev(points[i]);
   rt_status st = RT_OK;
@@ -286,13 +299,41 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   std::vector<int32_t> pp;
   if ((st = read_plan_inputs(sim, trace, stream, off, pp, "rt_sim_run_replicas")) != RT_OK) return st;
 
-  // Plan: bucket replicas by kernel class, longest replica first within a
-  // class so that long chains start early; empty replicas need no work.
+  // Plan.  Each point runs one kernel class.  With few replicas (fewer
+  // waves, at the shortest-step classes, than twice the GPU's SIMDs) every
+  // replica is a latency chain and takes the shortest-step class; with many,
+  // the GPU's issue rate is the limit and each point takes the segment class
+  // with the fewest issue slots per replica-step (lanes x step cost).  Then
+  // replicas are bucketed by class, longest first so that long chains start
+  // early; empty replicas need no work.
   const int ncls = rt::sim_class_count();
-  std::vector<std::vector<int32_t>> buckets(ncls);
   const int64_t n = trace->n_replicas;
+  const size_t npts = sim->points.size();
+  std::vector<int64_t> reps_of(npts, 0);
   for (int64_t i = 0; i < n; ++i)
-    if (off[i + 1] > off[i]) buckets[sim->point_class[pp[i]]].push_back((int32_t)i);
+    if (off[i + 1] > off[i]) reps_of[pp[i]] += 1;
+  double waves = 0.0;
+  for (size_t k = 0; k < npts; ++k) waves += (double)reps_of[k] * rt::sim_class(sim->point_classes[k][0]).S / 64.0;
+  const bool many = waves >= 2.0 * kSimds;
+  std::vector<int> choice(npts);
+  for (size_t k = 0; k < npts; ++k) {
+    const std::vector<int>& fit = sim->point_classes[k];
+    choice[k] = fit[0];
+    if (!many) continue;
+    double best = -1.0;
+    for (int c : fit) {
+      const rt::SimClass sc = rt::sim_class(c);
+      if (sc.kind != rt::kSeg) continue;
+      const double cost = sc.S * seg_step_cost(sc);
+      if (best < 0.0 || cost < best) {
+        best = cost;
+        choice[k] = c;
+      }
+    }
+  }
+  std::vector<std::vector<int32_t>> buckets(ncls);
+  for (int64_t i = 0; i < n; ++i)
+    if (off[i + 1] > off[i]) buckets[choice[pp[i]]].push_back((int32_t)i);
   for (auto& b : buckets)
     std::stable_sort(b.begin(), b.end(), [&](int32_t x, int32_t y) {
       return off[x + 1] - off[x] > off[y + 1] - off[y];
@@ -406,11 +447,14 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
       if ((e = hipStreamWaitEvent(where, sim->fork, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
     if ((e = rt::launch_sim(rt::sim_class(c), a, where)) != hipSuccess) return hip_fail(e, "launch(sim)");
-    if (act.size() > 1) {
-      if ((e = hipEventRecord(sim->joins[k], where)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-      if ((e = hipStreamWaitEvent(stream, sim->joins[k], 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
-    }
+    if (act.size() > 1 && (e = hipEventRecord(sim->joins[k], where)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   }
+  // The joins go in after every launch: streams share the device's few
+  // hardware queues, and a wait enqueued between two launches could hold
+  // back a later launch that landed on the same queue.
+  if (act.size() > 1)
+    for (size_t k = 0; k < act.size(); ++k)
+      if ((e = hipStreamWaitEvent(stream, sim->joins[k], 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
   if (sim->timing) {
     if ((e = hipEventRecord(sim->t1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     sim->timed_pending = true;

@@ -51,11 +51,15 @@
 // to right in float32, one rounding per operation (built with
 // -ffp-contract=off).  Times and token totals are integers held in doubles
 // (exact below 2^53; simulated times are kept below 2^52).
+#pragma once
+
+#include <algorithm>
+
 #include "lane_ops.h"
 #include "rt_internal.h"
 
 namespace rt {
-namespace {
+namespace seg {
 
 constexpr double kInf = __builtin_huge_val();
 
@@ -140,7 +144,8 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   const int lane = threadIdx.x & 63;
   const int sl = lane & (S - 1);
   const int segw = (int)(threadIdx.x >> 6) * kSegs + lane / S;  // segment within the block
-  const int64_t item = (int64_t)blockIdx.x * (kWaves * kSegs) + segw;
+  // a workgroup has 1 .. kWaves waves (chosen at launch)
+  const int64_t item = (int64_t)blockIdx.x * ((int64_t)(blockDim.x >> 6) * kSegs) + segw;
   const bool live = item < a.n_work;
   const int rep = live ? a.work[item] : 0;
   const int64_t base = live ? a.offsets[rep] : 0;
@@ -443,47 +448,34 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   if (flag) atomicOr(a.flag, flag);
 }
 
-// Four waves per workgroup (one per SIMD of a compute unit).
+// Up to four waves per workgroup (one per SIMD of a compute unit).  A launch
+// with few waves uses smaller workgroups, so that they spread over more
+// compute units (each unit's memory pipeline is shared by its waves).
 constexpr int kSegWaves = 4;
+constexpr int kComputeUnits = 256;
 
 template <int S, int M, int kMode>
 hipError_t launch_seg(const SimArgs& a, hipStream_t stream) {
   if (a.n_work <= 0) return hipSuccess;
-  const int64_t per_block = kSegWaves * (64 / S);
-  const int64_t blocks = (a.n_work + per_block - 1) / per_block;
-  hipLaunchKernelGGL((seg_kernel<S, M, kMode, kSegWaves>), dim3((unsigned)blocks), dim3(64 * kSegWaves), 0, stream,
+  constexpr int64_t kSegs = 64 / S;
+  const int64_t waves = (a.n_work + kSegs - 1) / kSegs;
+  const int64_t wpb = std::min<int64_t>(kSegWaves, std::max<int64_t>(1, (waves + kComputeUnits - 1) / kComputeUnits));
+  const int64_t blocks = (waves + wpb - 1) / wpb;
+  hipLaunchKernelGGL((seg_kernel<S, M, kMode, kSegWaves>), dim3((unsigned)blocks), dim3(64 * (unsigned)wpb), 0, stream,
                      a);
   return hipGetLastError();
 }
 
-struct SegEntry {
-  int S, M, mode;
-  hipError_t (*fn)(const SimArgs&, hipStream_t);
-};
+// The segment widths and lane depths compiled for every mode.
+#define RT_SEG_FOR_EACH(X)                                                    \
+  X(2, 1) X(4, 1) X(8, 1) X(16, 1) X(32, 1) X(64, 1) X(2, 2) X(4, 2) X(8, 2)  \
+  X(16, 2) X(32, 2) X(64, 2) X(2, 3) X(4, 3) X(8, 3) X(16, 3) X(32, 3)        \
+  X(64, 3) X(2, 4) X(4, 4) X(8, 4) X(16, 4) X(32, 4) X(64, 4)
 
-#define RT_SEG3(S, M)                                                                                \
-  {S, M, kModeTrue, launch_seg<S, M, kModeTrue>}, {S, M, kModeProxy, launch_seg<S, M, kModeProxy>}, \
-      {S, M, kModeBase, launch_seg<S, M, kModeBase>}
+// Launch the (S, M) kernel of one mode (defined in one source file per mode).
+template <int kMode>
+hipError_t launch_mode(int S, int M, const SimArgs& a, hipStream_t stream);
 
-// In order of preference: the fewest instances per lane, then the narrowest
-// segment that holds both pools.
-const SegEntry kSegTable[] = {RT_SEG3(2, 1),  RT_SEG3(4, 1),  RT_SEG3(8, 1),  RT_SEG3(16, 1),
-                              RT_SEG3(32, 1), RT_SEG3(64, 1), RT_SEG3(64, 2), RT_SEG3(64, 4)};
-#undef RT_SEG3
 
-}  // namespace
-
-int seg_class_count() { return (int)(sizeof(kSegTable) / sizeof(kSegTable[0])); }
-
-SimClass seg_class(int i) {
-  const SegEntry& e = kSegTable[i];
-  return SimClass{kSeg, e.S, e.M, e.M, e.mode};
-}
-
-hipError_t launch_seg_class(const SimClass& c, const SimArgs& a, hipStream_t stream) {
-  for (const SegEntry& e : kSegTable)
-    if (e.S == c.S && e.M == c.MP && e.mode == c.mode) return e.fn(a, stream);
-  return hipErrorInvalidValue;
-}
-
+}  // namespace seg
 }  // namespace rt

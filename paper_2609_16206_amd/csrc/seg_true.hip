@@ -1,0 +1,18 @@
+// Segment-kernel instances for the true scoring mode (one source file
+// per mode, so that they compile in parallel).
+#include "seg_kernel.h"
+
+namespace rt {
+namespace seg {
+
+#define RT_SEG_CASE(S_, M_) \
+  if (S == S_ && M == M_) return launch_seg<S_, M_, kModeTrue>(a, stream);
+
+template <>
+hipError_t launch_mode<kModeTrue>(int S, int M, const SimArgs& a, hipStream_t stream) {
+  RT_SEG_FOR_EACH(RT_SEG_CASE)
+  return hipErrorInvalidValue;
+}
+
+}  // namespace seg
+}  // namespace rt

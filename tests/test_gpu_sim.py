@@ -120,6 +120,25 @@ def test_simultaneous_arrivals_and_rejections():
     assert rep["invalid"] == int((gpu["ttft_ns"] < 0).sum())
 
 
+def test_many_replicas_packed_classes():
+    """Enough replicas that the planner packs several instances per lane (the
+    throughput classes), for every scoring mode and a spread of pool shapes."""
+    shapes = [(1, 2), (2, 3), (2, 6), (3, 9), (2, 16), (4, 30), (2, 64), (5, 50)]
+    modes = [("learned", "true"), ("learned", "proxy"), ("round_robin", "true"), ("least_loaded", "true")]
+    pts = [W.make_point(P, D, n_classes=3, policy=pol, backlog_mode=bm, kv_cap=20_000)
+           for (P, D) in shapes for (pol, bm) in modes]
+    n_rep, n_req = 24576, 48
+    lengths = [n_req - (i % 7) for i in range(n_rep)]
+    tr = _ragged_trace(pts, lengths, seed=31, rate_scale=1.1)
+    log(f"packed classes: {len(pts)} points, {n_rep} replicas, {tr['arrival_ns'].size} requests")
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    check_properties(pts, tr, gpu)
+    assert np.array_equal(goodput_recount(pts, tr, gpu), met)
+    rep = follow_replicas(pts, tr, gpu, range(n_rep), gpu_goodput=g, gpu_met=met)
+    log(f"packed classes: {rep}")
+
+
 def test_determinism_and_range_resume():
     wl = W.paper_cluster(n_replicas=300, requests=3000)
     tr = W.make_trace(wl)
