@@ -10,6 +10,7 @@
 
 #include "rt_internal.h"
 #include "rt_router.h"
+#include "wseg_kernel.h"
 
 namespace {
 
@@ -107,14 +108,20 @@ int point_mode(const rt_point& p) {
   return p.backlog_mode == RT_BACKLOG_TRUE ? rt::kModeTrue : rt::kModeProxy;
 }
 
-// Does kernel class c hold both pools of point p?  A segment class of the
-// point's mode needs ceil(P / M) prefill lanes and ceil(D / M) decode lanes
-// within its S; a wide class holds P <= S * MP and D <= S * MD.
+// Does kernel class c hold both pools of point p?  A one-wave segment class
+// of the point's mode needs ceil(P / M) prefill lanes and ceil(D / M) decode
+// lanes within its S; a multi-wave one needs every wave's share of both
+// within 64 lanes; a wide class holds P <= S * MP and D <= S * MD.
 bool class_fits(const rt::SimClass& c, const rt_point& p) {
   if (c.kind == rt::kSeg) {
     if (c.mode != point_mode(p)) return false;
     const int lanes = (p.n_prefill + c.MP - 1) / c.MP + (p.n_decode + c.MD - 1) / c.MD;
     return lanes <= c.S;
+  }
+  if (c.kind == rt::kWseg) {
+    if (c.mode != point_mode(p)) return false;
+    const int W = c.S / 64;
+    return rt::seg::wide_pool_lanes(p.n_prefill, c.MP, W) + rt::seg::wide_pool_lanes(p.n_decode, c.MD, W) <= 64;
   }
   return p.n_prefill <= c.S * c.MP && p.n_decode <= c.S * c.MD;
 }

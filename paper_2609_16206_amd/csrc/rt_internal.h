@@ -67,10 +67,10 @@ constexpr int kDummyLanes = 1 << 16;
 // Kernel classes.  kSeg: one replica per aligned segment of S <= 64 lanes of
 // one wave, prefill instances on the first lanes and decode instances on the
 // next, MP = MD instances per lane; `mode` fixes the scoring path (clock
-// backlog, ledger backlog, or a baseline policy).  kWide: S > 64 lanes (S/64
-// waves of one workgroup) hold MP prefill and MD decode instances each, any
-// mode.
-enum SimKind { kSeg = 0, kWide = 1 };
+// backlog, ledger backlog, or a baseline policy).  kWseg: the same for one
+// replica per workgroup of S / 64 waves.  kWide: the general kernel for any
+// mode, S > 64 lanes holding MP prefill and MD decode instances each.
+enum SimKind { kSeg = 0, kWide = 1, kWseg = 2 };
 enum SimMode { kModeTrue = 0, kModeProxy = 1, kModeBase = 2, kModeAny = 3 };
 
 struct SimClass {
@@ -83,7 +83,7 @@ hipError_t launch_sim(const SimClass& c, const SimArgs& a, hipStream_t stream);
 int sim_class_count();
 SimClass sim_class(int i);
 // the two families behind them
-int seg_class_count();
+int seg_class_count();  // kSeg and kWseg classes
 SimClass seg_class(int i);
 hipError_t launch_seg_class(const SimClass& c, const SimArgs& a, hipStream_t stream);
 int wide_class_count();

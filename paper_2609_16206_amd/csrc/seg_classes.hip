@@ -1,5 +1,6 @@
 // The segment-kernel classes: every (S, M) compiled, for each scoring mode.
 #include "seg_kernel.h"
+#include "wseg_kernel.h"
 
 namespace rt {
 namespace {
@@ -16,25 +17,38 @@ struct SegShape {
 const SegShape kShapes[] = {RT_SEG_FOR_EACH(RT_SEG_SHAPE)};
 #undef RT_SEG_SHAPE
 constexpr int kNumShapes = (int)(sizeof(kShapes) / sizeof(kShapes[0]));
+// Multi-wave segments: {waves, instances per lane}, after the one-wave ones.
+#define RT_WSEG_SHAPE(W_, M_) {W_, M_},
+const SegShape kWideShapes[] = {RT_WSEG_FOR_EACH(RT_WSEG_SHAPE)};
+#undef RT_WSEG_SHAPE
+constexpr int kNumWide = (int)(sizeof(kWideShapes) / sizeof(kWideShapes[0]));
 constexpr int kModes[] = {kModeTrue, kModeProxy, kModeBase};
 
 }  // namespace
 
-int seg_class_count() { return kNumShapes * 3; }
+int seg_class_count() { return (kNumShapes + kNumWide) * 3; }
 
 SimClass seg_class(int i) {
-  const SegShape& e = kShapes[i % kNumShapes];
-  return SimClass{kSeg, e.S, e.M, e.M, kModes[i / kNumShapes]};
+  if (i < kNumShapes * 3) {
+    const SegShape& e = kShapes[i % kNumShapes];
+    return SimClass{kSeg, e.S, e.M, e.M, kModes[i / kNumShapes]};
+  }
+  i -= kNumShapes * 3;
+  const SegShape& e = kWideShapes[i % kNumWide];
+  return SimClass{kWseg, 64 * e.S, e.M, e.M, kModes[i / kNumWide]};
 }
 
 hipError_t launch_seg_class(const SimClass& c, const SimArgs& a, hipStream_t stream) {
+  const bool w = c.kind == kWseg;
+  const int S = w ? c.S / 64 : c.S;
   switch (c.mode) {
     case kModeTrue:
-      return seg::launch_mode<kModeTrue>(c.S, c.MP, a, stream);
+      return w ? seg::launch_wide_mode<kModeTrue>(S, c.MP, a, stream) : seg::launch_mode<kModeTrue>(S, c.MP, a, stream);
     case kModeProxy:
-      return seg::launch_mode<kModeProxy>(c.S, c.MP, a, stream);
+      return w ? seg::launch_wide_mode<kModeProxy>(S, c.MP, a, stream)
+               : seg::launch_mode<kModeProxy>(S, c.MP, a, stream);
     case kModeBase:
-      return seg::launch_mode<kModeBase>(c.S, c.MP, a, stream);
+      return w ? seg::launch_wide_mode<kModeBase>(S, c.MP, a, stream) : seg::launch_mode<kModeBase>(S, c.MP, a, stream);
     default:
       return hipErrorInvalidValue;
   }

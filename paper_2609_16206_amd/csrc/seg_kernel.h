@@ -136,6 +136,87 @@ __device__ __forceinline__ void load_pair(Slot& s, const char* rp, const char* t
   }
 }
 
+// A request as the step sees it: checked, with its derived token sums.
+struct Req {
+  double now, now_eff;
+  int32_t p, o, oh, po, poh;
+  bool go;
+};
+
+// Request validity: lengths >= 1, token sums within int32, class in range,
+// the step belongs to the replica (rem >= 1), arrival >= 0 and not before
+// the last accepted one.  A rejected request is not routed and changes no
+// state; it releases nothing (now_eff = -1).
+__device__ __forceinline__ Req admit_check(int32_t rem, int32_t ncls, int64_t arr, int32_t p, int32_t o, int32_t oh,
+                                           uint32_t c, double& last_now) {
+  Req q;
+  q.p = p;
+  q.o = o;
+  q.oh = oh;
+  q.po = (int32_t)((uint32_t)p + (uint32_t)o);
+  q.poh = (int32_t)((uint32_t)p + (uint32_t)oh);
+  const int32_t vm = min(min(min(p, o), min(oh, q.po)), min(min(q.poh, ncls - (int32_t)c), rem));
+  q.now = i64_to_f64(arr);
+  const double xv = opaque(vm) >= 1 ? q.now : -1.0;
+  q.go = xv >= last_now;
+  q.now_eff = q.go ? xv : -1.0;
+  last_now = __builtin_fmax(last_now, xv);
+  return q;
+}
+
+// Release: up to two completions per instance from the register window; the
+// new head's successors are loaded unconditionally (the wave's dummy record
+// `dmy` when there is nothing to load) and merged later.
+template <bool kTok, bool kKv>
+__device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char* recb, const char* tokb, int64_t base,
+                                             int32_t R, int64_t dmy) {
+  const bool p1 = x.h.t <= now_eff;
+  const bool p2 = x.n.t <= now_eff;  // implies p1 (release times do not decrease)
+  x.q -= (p1 ? 1 : 0) + (p2 ? 1 : 0);
+  if constexpr (kKv) x.kv = x.kv - ((p1 ? (double)x.h.fp : 0.0) + (p2 ? (double)x.n.fp : 0.0));
+  if constexpr (kTok) x.pend = x.pend - ((p1 ? (double)x.h.pt : 0.0) + (p2 ? (double)x.n.pt : 0.0));
+  const Elem h1 = sel(p2, x.n2, sel(p1, x.n, x.h));
+  Elem n1 = sel(p1, x.n2, x.n);
+  n1.t = p2 ? kInf : n1.t;
+  x.h = h1;
+  x.n = n1;
+  x.n2.t = p1 ? kInf : x.n2.t;
+  const int32_t lq = opaque(p1 ? x.q : 0);
+  const bool ld = lq >= 2;
+  const int64_t g = ld ? base + min(max(x.h.idx, 0), max(R - 1, 0)) : dmy;
+  load_pair<kTok>(x, recb + g * kRecStride, tokb + g * kRecStride);
+  x.lq = lq;
+}
+
+template <int M, bool kTok, bool kKv>
+__device__ __forceinline__ void release_fast(Slot (&s)[M], double now_eff, const char* recb, const char* tokb,
+                                             int64_t base, int32_t R, int64_t dmy) {
+#pragma unroll
+  for (int m = 0; m < M; ++m) release_slot<kTok, kKv>(s[m], now_eff, recb, tokb, base, R, dmy);
+}
+
+template <int M>
+__device__ __forceinline__ double head_min(const Slot (&s)[M]) {
+  double h = s[0].h.t;
+#pragma unroll
+  for (int m = 1; m < M; ++m) h = __builtin_fmin(h, s[m].h.t);
+  return h;
+}
+
+// More completions than the window holds (rare): wait for the loaded
+// successors and release again, until no head of the wave has finished.
+template <int M, bool kTok, bool kKv>
+__device__ __forceinline__ void release_more(Slot (&s)[M], double now_eff, const char* recb, const char* tokb,
+                                             int64_t base, int32_t R, int64_t dmy) {
+  if (__builtin_expect(__any(head_min(s) <= now_eff), 0)) {
+    do {
+#pragma unroll
+      for (int m = 0; m < M; ++m) merge_pending(s[m]);
+      release_fast<M, kTok, kKv>(s, now_eff, recb, tokb, base, R, dmy);
+    } while (__any(head_min(s) <= now_eff));
+  }
+}
+
 template <int S, int M, int kMode, int kWaves>
 __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   constexpr bool kTok = kMode == kModeProxy;  // the ledger is priced
@@ -196,73 +277,9 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   const int32_t rd_last = R > 0 ? R - 1 : 0;
   double last_now = 0.0;  // latest accepted arrival (arrivals must not decrease)
 
-  // Request validity: lengths >= 1, token sums within int32, class in range,
-  // the step belongs to the replica, arrival >= 0 and not before the last
-  // accepted one.  A rejected request is not routed and changes no state; it
-  // releases nothing (now = -1).
-  struct Req {
-    double now, now_eff;
-    int32_t p, o, oh, po, poh;
-    bool go;
-  };
-  auto admit_check = [&](int32_t t, int64_t arr, int32_t p, int32_t o, int32_t oh, uint32_t c) {
-    Req q;
-    q.p = p;
-    q.o = o;
-    q.oh = oh;
-    q.po = (int32_t)((uint32_t)p + (uint32_t)o);
-    q.poh = (int32_t)((uint32_t)p + (uint32_t)oh);
-    const int32_t vm = min(min(min(p, o), min(oh, q.po)), min(min(q.poh, ncls - (int32_t)c), R - t));
-    q.now = i64_to_f64(arr);
-    const double xv = opaque(vm) >= 1 ? q.now : -1.0;
-    q.go = xv >= last_now;
-    q.now_eff = q.go ? xv : -1.0;
-    last_now = __builtin_fmax(last_now, xv);
-    return q;
-  };
-
-  // Release: up to two completions per instance from the register window;
-  // the new head's successors are loaded unconditionally (merged one step
-  // later).
-  auto release_fast = [&](double now_eff) {
-#pragma unroll
-    for (int m = 0; m < M; ++m) {
-      Slot& x = s[m];
-      const bool p1 = x.h.t <= now_eff;
-      const bool p2 = x.n.t <= now_eff;  // implies p1 (release times do not decrease)
-      x.q -= (p1 ? 1 : 0) + (p2 ? 1 : 0);
-      if constexpr (kKv) x.kv = x.kv - ((p1 ? (double)x.h.fp : 0.0) + (p2 ? (double)x.n.fp : 0.0));
-      if constexpr (kTok) x.pend = x.pend - ((p1 ? (double)x.h.pt : 0.0) + (p2 ? (double)x.n.pt : 0.0));
-      const Elem h1 = sel(p2, x.n2, sel(p1, x.n, x.h));
-      Elem n1 = sel(p1, x.n2, x.n);
-      n1.t = p2 ? kInf : n1.t;
-      x.h = h1;
-      x.n = n1;
-      x.n2.t = p1 ? kInf : x.n2.t;
-      const int32_t lq = opaque(p1 ? x.q : 0);
-      const bool ld = lq >= 2;
-      const int64_t g = ld ? base + min(max(x.h.idx, 0), max(R - 1, 0)) : dmy;
-      load_pair<kTok>(x, recb + g * kRecStride, tokb + g * kRecStride);
-      x.lq = lq;
-    }
-  };
-  // More completions than the window holds (rare): wait for the loaded
-  // successors and release again, until no head has finished.
   auto release = [&](double now_eff) {
-    release_fast(now_eff);
-    double hmin = s[0].h.t;
-#pragma unroll
-    for (int m = 1; m < M; ++m) hmin = __builtin_fmin(hmin, s[m].h.t);
-    if (__builtin_expect(__any(hmin <= now_eff), 0)) {
-      do {
-#pragma unroll
-        for (int m = 0; m < M; ++m) merge_pending(s[m]);
-        release_fast(now_eff);
-        hmin = s[0].h.t;
-#pragma unroll
-        for (int m = 1; m < M; ++m) hmin = __builtin_fmin(hmin, s[m].h.t);
-      } while (__any(hmin <= now_eff));
-    }
+    release_fast<M, kTok, kKv>(s, now_eff, recb, tokb, base, R, dmy);
+    release_more<M, kTok, kKv>(s, now_eff, recb, tokb, base, R, dmy);
   };
 
   // Raw features of one request as loaded.
@@ -421,7 +438,7 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     __builtin_amdgcn_sched_barrier(0);
 
     // 6. request t+1: check, sigma, releases; load request t+2
-    cur = admit_check(t + 1, nx.arr, nx.p, nx.o, nx.oh, nx.c);
+    cur = admit_check(R - (t + 1), ncls, nx.arr, nx.p, nx.o, nx.oh, nx.c, last_now);
     sg = sig[segw * kMaxClasses + (nx.c & (kMaxClasses - 1))];
     release(cur.now_eff);
     load_feat(ld, t + 2);
@@ -431,7 +448,7 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   Feat fa, fb;
   load_feat(fa, 0);
   __builtin_amdgcn_s_waitcnt(0);
-  cur = admit_check(0, fa.arr, fa.p, fa.o, fa.oh, fa.c);
+  cur = admit_check(R, ncls, fa.arr, fa.p, fa.o, fa.oh, fa.c, last_now);
   sg = sig[segw * kMaxClasses + (fa.c & (kMaxClasses - 1))];
   load_feat(fa, 1);
   // enter the loop with nothing in flight, so that the loop header needs no

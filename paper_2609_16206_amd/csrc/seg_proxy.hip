@@ -1,6 +1,7 @@
-// Segment-kernel instances for the proxy scoring mode (one source file
-// per mode, so that they compile in parallel).
+// Segment-kernel and wide-segment-kernel instances for the proxy scoring
+// mode (one source file per mode, so that they compile in parallel).
 #include "seg_kernel.h"
+#include "wseg_kernel.h"
 
 namespace rt {
 namespace seg {
@@ -11,6 +12,15 @@ namespace seg {
 template <>
 hipError_t launch_mode<kModeProxy>(int S, int M, const SimArgs& a, hipStream_t stream) {
   RT_SEG_FOR_EACH(RT_SEG_CASE)
+  return hipErrorInvalidValue;
+}
+
+#define RT_WSEG_CASE(W_, M_) \
+  if (W == W_ && M == M_) return launch_wseg<W_, M_, kModeProxy>(a, stream);
+
+template <>
+hipError_t launch_wide_mode<kModeProxy>(int W, int M, const SimArgs& a, hipStream_t stream) {
+  RT_WSEG_FOR_EACH(RT_WSEG_CASE)
   return hipErrorInvalidValue;
 }
 

@@ -575,7 +575,7 @@ int sim_class_count() { return seg_class_count() + wide_class_count(); }
 SimClass sim_class(int i) { return i < seg_class_count() ? seg_class(i) : wide_class(i - seg_class_count()); }
 
 hipError_t launch_sim(const SimClass& c, const SimArgs& a, hipStream_t stream) {
-  return c.kind == kSeg ? launch_seg_class(c, a, stream) : launch_wide_class(c, a, stream);
+  return c.kind == kWide ? launch_wide_class(c, a, stream) : launch_seg_class(c, a, stream);
 }
 
 }  // namespace rt
