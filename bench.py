@@ -59,7 +59,7 @@ def _source_hash(files):
 
 
 SIM_SOURCES = ["paper_2609_16206_amd/csrc/" + f for f in (
-    "seg_kernel.h", "wseg_kernel.h", "seg_true.hip", "seg_proxy.hip", "seg_base.hip", "seg_classes.hip", "sim_kernel.hip",
+    "seg_kernel.h", "wseg_kernel.h", "seg_true.hip", "seg_proxy.hip", "seg_base.hip", "seg_classes.hip",
     "lane_ops.h", "rt_internal.h")]
 SCORE_SOURCES = ["paper_2609_16206_amd/csrc/score_kernel.hip", "paper_2609_16206_amd/csrc/rt_internal.h"]
 

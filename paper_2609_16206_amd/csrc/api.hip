@@ -111,19 +111,16 @@ int point_mode(const rt_point& p) {
 // Does kernel class c hold both pools of point p?  A one-wave segment class
 // of the point's mode needs ceil(P / M) prefill lanes and ceil(D / M) decode
 // lanes within its S; a multi-wave one needs every wave's share of both
-// within 64 lanes; a wide class holds P <= S * MP and D <= S * MD.
+// within 64 lanes.
 bool class_fits(const rt::SimClass& c, const rt_point& p) {
   if (c.kind == rt::kSeg) {
     if (c.mode != point_mode(p)) return false;
     const int lanes = (p.n_prefill + c.MP - 1) / c.MP + (p.n_decode + c.MD - 1) / c.MD;
     return lanes <= c.S;
   }
-  if (c.kind == rt::kWseg) {
-    if (c.mode != point_mode(p)) return false;
-    const int W = c.S / 64;
-    return rt::seg::wide_pool_lanes(p.n_prefill, c.MP, W) + rt::seg::wide_pool_lanes(p.n_decode, c.MD, W) <= 64;
-  }
-  return p.n_prefill <= c.S * c.MP && p.n_decode <= c.S * c.MD;
+  if (c.mode != point_mode(p)) return false;
+  const int W = c.S / 64;
+  return rt::seg::wide_pool_lanes(p.n_prefill, c.MP, W) + rt::seg::wide_pool_lanes(p.n_decode, c.MD, W) <= 64;
 }
 
 // Every class that holds a point, in the order the classes are listed (the

@@ -68,27 +68,20 @@ constexpr int kDummyLanes = 1 << 16;
 // one wave, prefill instances on the first lanes and decode instances on the
 // next, MP = MD instances per lane; `mode` fixes the scoring path (clock
 // backlog, ledger backlog, or a baseline policy).  kWseg: the same for one
-// replica per workgroup of S / 64 waves.  kWide: the general kernel for any
-// mode, S > 64 lanes holding MP prefill and MD decode instances each.
-enum SimKind { kSeg = 0, kWide = 1, kWseg = 2 };
-enum SimMode { kModeTrue = 0, kModeProxy = 1, kModeBase = 2, kModeAny = 3 };
+// replica per workgroup of S / 64 waves, instances dealt round-robin over the
+// waves.
+enum SimKind { kSeg = 0, kWseg = 1 };
+enum SimMode { kModeTrue = 0, kModeProxy = 1, kModeBase = 2 };
 
 struct SimClass {
   int kind, S, MP, MD, mode;
 };
 
-// Every kernel class, segment classes first (in order of preference), and
+// Every kernel class, one-wave classes first (in order of preference), and
 // the launch of one class over a work list.
 hipError_t launch_sim(const SimClass& c, const SimArgs& a, hipStream_t stream);
 int sim_class_count();
 SimClass sim_class(int i);
-// the two families behind them
-int seg_class_count();  // kSeg and kWseg classes
-SimClass seg_class(int i);
-hipError_t launch_seg_class(const SimClass& c, const SimArgs& a, hipStream_t stream);
-int wide_class_count();
-SimClass wide_class(int i);
-hipError_t launch_wide_class(const SimClass& c, const SimArgs& a, hipStream_t stream);
 
 struct ScoreArgs {
   float w_b, w_s, w_q, rho, tau, inv_cap;

@@ -26,9 +26,9 @@ constexpr int kModes[] = {kModeTrue, kModeProxy, kModeBase};
 
 }  // namespace
 
-int seg_class_count() { return (kNumShapes + kNumWide) * 3; }
+int sim_class_count() { return (kNumShapes + kNumWide) * 3; }
 
-SimClass seg_class(int i) {
+SimClass sim_class(int i) {
   if (i < kNumShapes * 3) {
     const SegShape& e = kShapes[i % kNumShapes];
     return SimClass{kSeg, e.S, e.M, e.M, kModes[i / kNumShapes]};
@@ -38,7 +38,7 @@ SimClass seg_class(int i) {
   return SimClass{kWseg, 64 * e.S, e.M, e.M, kModes[i / kNumWide]};
 }
 
-hipError_t launch_seg_class(const SimClass& c, const SimArgs& a, hipStream_t stream) {
+hipError_t launch_sim(const SimClass& c, const SimArgs& a, hipStream_t stream) {
   const bool w = c.kind == kWseg;
   const int S = w ? c.S / 64 : c.S;
   switch (c.mode) {

@@ -81,6 +81,24 @@ def test_mixed_shapes_ragged_lengths():
     assert np.all(g[np.array(lengths) == 0] == 0.0)
 
 
+def test_pools_at_the_limit():
+    """Pools of RT_MAX_POOL instances, and lopsided ones, in every scoring
+    mode: each takes a multi-wave class."""
+    shapes = [(1024, 1024), (1024, 1), (1, 1024), (1024, 700), (513, 1024), (900, 901)]
+    pts = []
+    for k, (P, D) in enumerate(shapes):
+        pol = ("learned", "learned", "round_robin")[k % 3]
+        mode = ("true", "proxy")[k % 2]
+        pts.append(W.make_point(P, D, n_classes=3, policy=pol, backlog_mode=mode, kv_cap=50_000))
+    lengths = [3000, 1, 2000, 0, 2500, 1500, 65, 4000, 700, 3]
+    tr = _ragged_trace(pts, lengths, seed=17, rate_scale=1.5)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    check_properties(pts, tr, gpu)
+    rep = follow_replicas(pts, tr, gpu, range(len(lengths)), gpu_goodput=g, gpu_met=met)
+    log(f"pools at the limit: {rep}")
+
+
 def test_overload_deep_queues():
     """Arrivals at 3x capacity: long FIFOs, many pops per step."""
     pts = [W.make_point(2, 3, n_classes=3), W.make_point(2, 6, n_classes=3, backlog_mode="proxy"),
