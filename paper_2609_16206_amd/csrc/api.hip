@@ -344,15 +344,11 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
     });
 
   hipError_t e;
-  // Scratch: successor records (kRecStride bytes per request) and the dummy
-  // slots.
+  // Scratch: the dummy records, then the successor records (kRecStride
+  // bytes each).
   const size_t nreq = (size_t)trace->n_requests;
-  // (the dummy area also holds the wave-private dummy records at negative
-  // request indices, kDummyLanes / 64 of kRecStride bytes, right before the
-  // records)
-  const size_t dummy_bytes = (size_t)rt::kDummyLanes * 64;
-  static_assert((size_t)rt::kDummyLanes * 64 >= (size_t)(rt::kDummyLanes / 64) * rt::kRecStride * 2,
-                "dummy area too small for the dummy records");
+  const size_t dummy_bytes = (size_t)rt::kDummyRecords * rt::kRecStride;
+  static_assert(((size_t)rt::kDummyRecords * rt::kRecStride) % 256 == 0, "records stay 256-byte aligned");
   const size_t need = nreq * rt::kRecStride + dummy_bytes + 256;
   if (need > sim->scratch_bytes) {
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
@@ -411,7 +407,6 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   a.i_dec = out->i_dec;
   a.ttft = out->ttft_ns;
   a.span = out->decode_span_ns;
-  a.dummy = sc;
   a.rec = sc + dummy_bytes;
   a.flag = sim->d_flag;
   if (sim->timing) {

@@ -36,6 +36,69 @@ __device__ __forceinline__ T opaque(T x) {
 }
 
 // ---------------------------------------------------------------------------
+// Stores on a subset of a wave's lanes.  A vector store sends one L2 write
+// request per active lane whatever its address (lanes that write one shared
+// dummy slot are not merged), so a store made by one lane in eight through a
+// dummy address costs as many requests as a full store.  These helpers switch
+// exec to the lanes whose condition is nonzero for the store alone and
+// restore it, inside one asm statement, so the compiler never sees exec
+// change.  They keep five wait states after the vector compare that writes
+// exec, and the exec restore after a 16-byte store is the wait state its data
+// registers need before they may be rewritten.  Addresses must be valid on
+// every lane all the same.
+//
+// The compiler does not count these stores in its memory-counter waits; a
+// wait it places for a load issued before one of them therefore also waits
+// for that store.  Callers issue them after the waits of their step.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void store_x4_if(uint32_t c, void* p, u32x4 v) {
+  uint64_t sv;
+  asm volatile(
+      "s_mov_b64 %0, exec\n\t"
+      "v_cmpx_ne_u32_e32 vcc, 0, %1\n\t"
+      "s_nop 4\n\t"
+      "global_store_dwordx4 %2, %3, off\n\t"
+      "s_mov_b64 exec, %0"
+      : "=&s"(sv)
+      : "v"(c), "v"(p), "v"(v)
+      : "vcc", "memory");
+}
+
+// 16 bytes at p and 4 bytes at q under one condition.
+__device__ __forceinline__ void store_x4_b32_if(uint32_t c, void* p, u32x4 v, void* q, uint32_t w) {
+  uint64_t sv;
+  asm volatile(
+      "s_mov_b64 %0, exec\n\t"
+      "v_cmpx_ne_u32_e32 vcc, 0, %1\n\t"
+      "s_nop 4\n\t"
+      "global_store_dwordx4 %2, %3, off\n\t"
+      "global_store_dword %4, %5, off\n\t"
+      "s_mov_b64 exec, %0"
+      : "=&s"(sv)
+      : "v"(c), "v"(p), "v"(v), "v"(q), "v"(w)
+      : "vcc", "memory");
+}
+
+// Two 4-byte and two 8-byte values (one simulated request's outcome).
+__device__ __forceinline__ void store_out_if(uint32_t c, int32_t* p0, int32_t v0, int32_t* p1, int32_t v1, int64_t* p2,
+                                             int64_t v2, int64_t* p3, int64_t v3) {
+  uint64_t sv;
+  asm volatile(
+      "s_mov_b64 %0, exec\n\t"
+      "v_cmpx_ne_u32_e32 vcc, 0, %1\n\t"
+      "s_nop 4\n\t"
+      "global_store_dword %2, %3, off\n\t"
+      "global_store_dword %4, %5, off\n\t"
+      "global_store_dwordx2 %6, %7, off\n\t"
+      "global_store_dwordx2 %8, %9, off\n\t"
+      "s_mov_b64 exec, %0"
+      : "=&s"(sv)
+      : "v"(c), "v"(p0), "v"(v0), "v"(p1), "v"(v1), "v"(p2), "v"(v2), "v"(p3), "v"(v3)
+      : "vcc", "memory");
+}
+
+// ---------------------------------------------------------------------------
 // Segment collectives over aligned groups of S lanes.  Within a 16-lane row:
 // quad_perm xor 1, xor 2, then half-row mirror and row mirror (each step
 // pairs every lane with one from the other half of its group, so after

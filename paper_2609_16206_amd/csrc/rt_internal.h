@@ -45,24 +45,24 @@ struct SimArgs {
   int64_t* span;
   // Successor records of the per-instance FIFOs: kRecStride bytes per
   // request, indexed by the global request index of the predecessor (see
-  // the offsets below).
+  // the offsets below).  kDummyRecords more records lie right before `rec`,
+  // at indices -1 .. -kDummyRecords: wave-private targets of record loads
+  // with nothing to load.
   char* rec;
-  char* dummy;  // kDummyLanes / 64 wave-private 64-byte slots (memory ops with nothing to do)
   uint32_t* flag;
 };
 
 // Layout of one request's scratch region.  For each pool, a pair of entries
 // {release time (double), index, cache tokens} describing the request's
 // first and second successor in the same instance's FIFO, and a pair of the
-// same successors' ledger tokens.  Kernels that keep one successor use the
-// first entry of each pair only.
+// same successors' ledger tokens.
 constexpr int kRecStride = 80;
 constexpr int kRecPairPre = 0;   // 2 x 16 bytes
 constexpr int kRecPairDec = 32;  // 2 x 16 bytes
 constexpr int kRecTokPre = 64;   // 2 x 4 bytes
 constexpr int kRecTokDec = 72;   // 2 x 4 bytes
 
-constexpr int kDummyLanes = 1 << 16;
+constexpr int kDummyRecords = 1024;  // a power of two
 
 // Kernel classes.  kSeg: one replica per aligned segment of S <= 64 lanes of
 // one wave, prefill instances on the first lanes and decode instances on the

@@ -124,6 +124,17 @@ __device__ __forceinline__ void pin_window(const Slot& s) {
                : "memory");
 }
 
+// Byte offset of request g's record region, g * kRecStride: g * 5 in one
+// 64-bit shift-add (written out, since the compiler would otherwise turn it
+// into two 32-bit multiply-adds), then * 16, which folds into the address
+// add.
+__device__ __forceinline__ int64_t rec_off(int64_t g) {
+  static_assert(kRecStride == 80, "rec_off assumes 80-byte records");
+  int64_t g5;
+  asm("v_lshl_add_u64 %0, %1, 2, %1" : "=v"(g5) : "v"(g));
+  return g5 << 4;
+}
+
 template <bool kTok>
 __device__ __forceinline__ void load_pair(Slot& s, const char* rp, const char* tp) {
   const EntryPair e = *reinterpret_cast<const EntryPair*>(rp);
@@ -184,7 +195,8 @@ __device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char
   const int32_t lq = opaque(p1 ? x.q : 0);
   const bool ld = lq >= 2;
   const int64_t g = ld ? base + min(max(x.h.idx, 0), max(R - 1, 0)) : dmy;
-  load_pair<kTok>(x, recb + g * kRecStride, tokb + g * kRecStride);
+  const int64_t go = rec_off(g);
+  load_pair<kTok>(x, recb + go, tokb + go);
   x.lq = lq;
 }
 
@@ -203,12 +215,24 @@ __device__ __forceinline__ double head_min(const Slot (&s)[M]) {
   return h;
 }
 
-// More completions than the window holds (rare): wait for the loaded
+// The earliest third FIFO position of the lane's slots.  Before the fast
+// releases, "some lane's third position has finished" is exactly "some head
+// has finished after them" (release times do not decrease along a FIFO).
+template <int M>
+__device__ __forceinline__ double third_min(const Slot (&s)[M]) {
+  double h = s[0].n2.t;
+#pragma unroll
+  for (int m = 1; m < M; ++m) h = __builtin_fmin(h, s[m].n2.t);
+  return h;
+}
+
+// More completions than the window holds (rare; `more` says that some head
+// of the wave has finished after the fast releases): wait for the loaded
 // successors and release again, until no head of the wave has finished.
 template <int M, bool kTok, bool kKv>
-__device__ __forceinline__ void release_more(Slot (&s)[M], double now_eff, const char* recb, const char* tokb,
-                                             int64_t base, int32_t R, int64_t dmy) {
-  if (__builtin_expect(__any(head_min(s) <= now_eff), 0)) {
+__device__ __forceinline__ void release_more(bool more, Slot (&s)[M], double now_eff, const char* recb,
+                                             const char* tokb, int64_t base, int32_t R, int64_t dmy) {
+  if (__builtin_expect(more, 0)) {
     do {
 #pragma unroll
       for (int m = 0; m < M; ++m) merge_pending(s[m]);
@@ -247,12 +271,14 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   char* const recb = a.rec + (isp ? kRecPairPre : kRecPairDec);
   char* const tokb = a.rec + (isp ? kRecTokPre : kRecTokDec);
   // The wave's dummy record: a negative request index whose region lies in
-  // the dummy area just before the records (record loads and stores with
-  // nothing to do use it, so that only an index is selected); and the wave's
-  // 64-byte dummy slot for output stores with nothing to write.
-  const uint32_t wave_id = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) & (kDummyLanes / 64 - 1);
+  // the dummy area just before the records.  Record loads and stores with
+  // nothing to do use it, so that only an index is selected; output stores
+  // with nothing to write go to its first 24 bytes.  (Stores stay
+  // unconditional: each lane of a store sends its own L2 request, but
+  // switching exec off and on around the store costs more issue time here.)
+  const uint32_t wave_id = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) & (kDummyRecords - 1);
   const int64_t dmy = -1 - (int64_t)wave_id;
-  char* const dummy = a.dummy + (size_t)wave_id * 64;
+  char* const dummy = a.rec + dmy * kRecStride;
 
   // sigma per class of each segment's point, read a step ahead of its use
   __shared__ float sig[kWaves * kSegs * kMaxClasses];
@@ -276,11 +302,6 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   const int64_t rd_base = R > 0 ? base : 0;
   const int32_t rd_last = R > 0 ? R - 1 : 0;
   double last_now = 0.0;  // latest accepted arrival (arrivals must not decrease)
-
-  auto release = [&](double now_eff) {
-    release_fast<M, kTok, kKv>(s, now_eff, recb, tokb, base, R, dmy);
-    release_more<M, kTok, kKv>(s, now_eff, recb, tokb, base, R, dmy);
-  };
 
   // Raw features of one request as loaded.
   struct Feat {
@@ -407,11 +428,12 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
       const Entry ze{end, t, fp};
       const bool s1 = opaque(st1) >= 0, s2 = opaque(st2) >= 0;
       const int64_t g1 = s1 ? base + st1 : dmy, g2 = s2 ? base + st2 : dmy;
-      *reinterpret_cast<Entry*>(recb + g1 * kRecStride) = ze;
-      *reinterpret_cast<Entry*>(recb + g2 * kRecStride + 16) = ze;
+      const int64_t o1 = rec_off(g1), o2 = rec_off(g2);
+      *reinterpret_cast<Entry*>(recb + o1) = ze;
+      *reinterpret_cast<Entry*>(recb + o2 + 16) = ze;
       if constexpr (kTok) {
-        *reinterpret_cast<int32_t*>(tokb + g1 * kRecStride) = tk;
-        *reinterpret_cast<int32_t*>(tokb + g2 * kRecStride + 4) = tk;
+        *reinterpret_cast<int32_t*>(tokb + o1) = tk;
+        *reinterpret_cast<int32_t*>(tokb + o2 + 4) = tk;
       }
       const int64_t go_i = base + t;
       int32_t* const d_ip = own_out ? a.i_pre + go_i : reinterpret_cast<int32_t*>(dummy);
@@ -437,10 +459,14 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     asm volatile("" : "+v"(nx.arr), "+v"(nx.p), "+v"(nx.o), "+v"(nx.oh), "+v"(nx.c));
     __builtin_amdgcn_sched_barrier(0);
 
-    // 6. request t+1: check, sigma, releases; load request t+2
+    // 6. request t+1: check, sigma, releases (the test for a slow path is
+    // made ahead of the fast releases, so that the scalar branch does not
+    // wait for its vector compare); load request t+2
     cur = admit_check(R - (t + 1), ncls, nx.arr, nx.p, nx.o, nx.oh, nx.c, last_now);
     sg = sig[segw * kMaxClasses + (nx.c & (kMaxClasses - 1))];
-    release(cur.now_eff);
+    const bool more = __any(third_min(s) <= cur.now_eff);
+    release_fast<M, kTok, kKv>(s, cur.now_eff, recb, tokb, base, R, dmy);
+    release_more<M, kTok, kKv>(more, s, cur.now_eff, recb, tokb, base, R, dmy);
     load_feat(ld, t + 2);
   };
 
@@ -457,9 +483,12 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
 
   // two steps per iteration, so that the features loaded in one step are
   // read in the next from the same registers
-  for (int32_t t = 0; __builtin_amdgcn_readfirstlane(t) < Rmax; t += 2) {
+  // (the count of steps left is a scalar, so the loop tests read no vector
+  // register)
+  int32_t t = 0;
+  for (int32_t left = Rmax; left > 0; left -= 2, t += 2) {
     step(t, fa, fb);
-    if (__builtin_amdgcn_readfirstlane(t) + 1 < Rmax) step(t + 1, fb, fa);
+    if (left > 1) step(t + 1, fb, fa);
   }
   const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u);
   if (flag) atomicOr(a.flag, flag);

@@ -63,9 +63,8 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   const double dec_tok_ns = (double)pt.dec_tok_ns, xfer_tok_ns = (double)pt.xfer_tok_ns;
   char* const recb = a.rec + (isp ? kRecPairPre : kRecPairDec);
   char* const tokb = a.rec + (isp ? kRecTokPre : kRecTokDec);
-  const uint32_t wave_id = (blockIdx.x * W + wave) & (kDummyLanes / 64 - 1);
+  const uint32_t wave_id = (blockIdx.x * W + wave) & (kDummyRecords - 1);
   const int64_t dmy = -1 - (int64_t)wave_id;  // the wave's dummy record
-  char* const dummy = a.dummy + (size_t)wave_id * 64;
 
   struct Part {
     uint32_t kp, kd;  // the wave's best prefill / decode key
@@ -194,10 +193,26 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     for (int m = 0; m < M; ++m)
       if (__any(s[m].lq >= 2)) merge_pending(s[m]);
 
-    // 5. append the request to the winning slot of each pool (uniform
-    // branches: the winner's wave, the winner's slot), record the outcome
+    // 5. request t+1: check and sigma (its features are waited for here,
+    // ahead of the stores below, which the compiler's waits do not count)
+    const Req nxt = [&] {
+      // (uniform over the workgroup; reading the first lane tells the compiler)
+      const int64_t u_arr = ((int64_t)__builtin_amdgcn_readfirstlane((int32_t)(nx_arr >> 32)) << 32) |
+                            (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)nx_arr);
+      const uint32_t u_c = (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)nx_c);
+      sg = sig[u_c & (kMaxClasses - 1)];
+      return admit_check(R - (t + 1), ncls, u_arr, __builtin_amdgcn_readfirstlane(nx_p),
+                         __builtin_amdgcn_readfirstlane(nx_o), __builtin_amdgcn_readfirstlane(nx_oh), u_c, last_now);
+    }();
+
+    // 6. append the request to the winning slot of each pool (uniform
+    // branches: the winner's wave, the winner's slot) and record the outcome;
+    // only the lanes with something to store store it.  Addresses are valid
+    // on every lane: a tail is >= -1, and index -1 lies in the dummy area
+    // before the records.
     if (go && wave == wpo) {
       const Elem z{pf_end, t, p, p};
+      const u32x4 zv = {(uint32_t)__double2loint(pf_end), (uint32_t)__double2hiint(pf_end), (uint32_t)t, (uint32_t)p};
 #pragma unroll
       for (int m = 0; m < M; ++m)
         if (m == mp) {
@@ -207,20 +222,20 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           x.h = sel(w == 0, z, x.h);
           x.n = sel(w == 1, z, x.n);
           x.n2 = sel(w == 2, z, x.n2);
-          const int64_t g1 = opaque(w) >= 1 ? base + x.tail : dmy;
-          const int64_t g2 = opaque(w) >= 2 ? base + x.tail2 : dmy;
+          const uint32_t s1 = opaque(w) >= 1 ? 1u : 0u, s2 = opaque(w) >= 2 ? 1u : 0u;
+          const int64_t g1 = base + x.tail, g2 = base + x.tail2;
           x.tail2 = own ? x.tail : x.tail2;
           x.tail = own ? t : x.tail;
           x.q = own ? x.q + 1 : x.q;
           if constexpr (kKv) x.kv = x.kv + (own ? (double)p : 0.0);
           if constexpr (kTok) x.pend = x.pend + (own ? (double)p : 0.0);
           x.busy = own ? pf_end : x.busy;
-          const Entry ze{pf_end, t, p};
-          *reinterpret_cast<Entry*>(recb + g1 * kRecStride) = ze;
-          *reinterpret_cast<Entry*>(recb + g2 * kRecStride + 16) = ze;
           if constexpr (kTok) {
-            *reinterpret_cast<int32_t*>(tokb + g1 * kRecStride) = p;
-            *reinterpret_cast<int32_t*>(tokb + g2 * kRecStride + 4) = p;
+            store_x4_b32_if(s1, recb + rec_off(g1), zv, tokb + rec_off(g1), (uint32_t)p);
+            store_x4_b32_if(s2, recb + rec_off(g2) + 16, zv, tokb + rec_off(g2) + 4, (uint32_t)p);
+          } else {
+            store_x4_if(s1, recb + rec_off(g1), zv);
+            store_x4_if(s2, recb + rec_off(g2) + 16, zv);
           }
         }
     }
@@ -236,64 +251,45 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           x.h = sel(w == 0, z, x.h);
           x.n = sel(w == 1, z, x.n);
           x.n2 = sel(w == 2, z, x.n2);
-          const int64_t g1 = opaque(w) >= 1 ? base + x.tail : dmy;
-          const int64_t g2 = opaque(w) >= 2 ? base + x.tail2 : dmy;
+          const uint32_t s1 = opaque(w) >= 1 ? 1u : 0u, s2 = opaque(w) >= 2 ? 1u : 0u;
+          const int64_t g1 = base + x.tail, g2 = base + x.tail2;
           x.tail2 = own ? x.tail : x.tail2;
           x.tail = own ? t : x.tail;
           x.q = own ? x.q + 1 : x.q;
           if constexpr (kKv) x.kv = x.kv + (own ? (double)po : 0.0);
           if constexpr (kTok) x.pend = x.pend + (own ? (double)oh : 0.0);
           x.busy = own ? de : x.busy;
-          const Entry ze{de, t, po};
-          *reinterpret_cast<Entry*>(recb + g1 * kRecStride) = ze;
-          *reinterpret_cast<Entry*>(recb + g2 * kRecStride + 16) = ze;
+          const u32x4 zv = {(uint32_t)__double2loint(de), (uint32_t)__double2hiint(de), (uint32_t)t, (uint32_t)po};
           if constexpr (kTok) {
-            *reinterpret_cast<int32_t*>(tokb + g1 * kRecStride) = oh;
-            *reinterpret_cast<int32_t*>(tokb + g2 * kRecStride + 4) = oh;
+            store_x4_b32_if(s1, recb + rec_off(g1), zv, tokb + rec_off(g1), (uint32_t)oh);
+            store_x4_b32_if(s2, recb + rec_off(g2) + 16, zv, tokb + rec_off(g2) + 4, (uint32_t)oh);
+          } else {
+            store_x4_if(s1, recb + rec_off(g1), zv);
+            store_x4_if(s2, recb + rec_off(g2) + 16, zv);
           }
           // the outcome, by the decode winner
           tmax = __builtin_fmax(tmax, own ? de : 0.0);
           const int64_t go_i = base + t;
-          int32_t* const d_ip = own ? a.i_pre + go_i : reinterpret_cast<int32_t*>(dummy);
-          int32_t* const d_id = own ? a.i_dec + go_i : reinterpret_cast<int32_t*>(dummy + 4);
-          int64_t* const d_tt = own ? a.ttft + go_i : reinterpret_cast<int64_t*>(dummy + 8);
-          int64_t* const d_sp = own ? a.span + go_i : reinterpret_cast<int64_t*>(dummy + 16);
-          *d_ip = ip;
-          *d_id = id;
-          *d_tt = f64_to_i64(pf_end - now);
-          *d_sp = f64_to_i64(de - pf_end);
+          store_out_if(own ? 1u : 0u, a.i_pre + go_i, ip, a.i_dec + go_i, id, a.ttft + go_i, f64_to_i64(pf_end - now),
+                       a.span + go_i, f64_to_i64(de - pf_end));
         }
     }
     if (!go && wave == 0) {
       // a rejected request: -1 outputs, by lane 0
       rej |= lane == 0 ? 1u : 0u;
       const int64_t go_i = base + t;
-      int32_t* const d_ip = lane == 0 ? a.i_pre + go_i : reinterpret_cast<int32_t*>(dummy);
-      int32_t* const d_id = lane == 0 ? a.i_dec + go_i : reinterpret_cast<int32_t*>(dummy + 4);
-      int64_t* const d_tt = lane == 0 ? a.ttft + go_i : reinterpret_cast<int64_t*>(dummy + 8);
-      int64_t* const d_sp = lane == 0 ? a.span + go_i : reinterpret_cast<int64_t*>(dummy + 16);
-      *d_ip = -1;
-      *d_id = -1;
-      *d_tt = -1;
-      *d_sp = -1;
+      store_out_if(lane == 0 ? 1u : 0u, a.i_pre + go_i, -1, a.i_dec + go_i, -1, a.ttft + go_i, (int64_t)-1,
+                   a.span + go_i, (int64_t)-1);
     }
     if constexpr (kMode == kModeBase) rr = (rr + 1 == npool) ? 0 : rr + 1;
 
-    // 6. request t+1: check, sigma, releases (slot by slot, where some
-    // lane's head has finished); load request t+2
-    {
-      // (uniform over the workgroup; reading the first lane tells the compiler)
-      const int64_t u_arr = ((int64_t)__builtin_amdgcn_readfirstlane((int32_t)(nx_arr >> 32)) << 32) |
-                            (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)nx_arr);
-      const uint32_t u_c = (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)nx_c);
-      cur = admit_check(R - (t + 1), ncls, u_arr, __builtin_amdgcn_readfirstlane(nx_p),
-                        __builtin_amdgcn_readfirstlane(nx_o), __builtin_amdgcn_readfirstlane(nx_oh), u_c, last_now);
-      sg = sig[u_c & (kMaxClasses - 1)];
-    }
+    // 7. the releases for request t+1 (slot by slot, where some lane's head
+    // has finished); load request t+2
+    cur = nxt;
 #pragma unroll
     for (int m = 0; m < M; ++m)
       if (__any(s[m].h.t <= cur.now_eff)) release_slot<kTok, kKv>(s[m], cur.now_eff, recb, tokb, base, R, dmy);
-    release_more<M, kTok, kKv>(s, cur.now_eff, recb, tokb, base, R, dmy);
+    release_more<M, kTok, kKv>(__any(head_min(s) <= cur.now_eff), s, cur.now_eff, recb, tokb, base, R, dmy);
     {
       const int64_t g = base + min(t + 2, last);
       nx_arr = a.arrival[g];
