@@ -52,7 +52,17 @@ def _cost(pt: Dict, backlog: np.float32, work: np.float32, sg: np.float32, kv: i
     return load + size + F(pt["w_q"]) * F(q)
 
 
-def simulate(pt: Dict, arrival, prompt, out, pred, cls) -> Dict[str, np.ndarray]:
+def _pair(u: int, v: int, n: int):
+    """The sampled policy's two candidates among n instances from words u, v:
+    u picks one of the n, v one of the n - 1 others (counted past the first)."""
+    a = (int(u) * n) >> 32
+    if n < 2:
+        return a, a
+    b = (int(v) * (n - 1)) >> 32
+    return a, (b if b < a else b + 1)
+
+
+def simulate(pt: Dict, arrival, prompt, out, pred, cls, words=None) -> Dict[str, np.ndarray]:
     n = len(arrival)
     P, D = int(pt["n_prefill"]), int(pt["n_decode"])
     s_pre = [int(pt["pre_base_ns"]) + int(prompt[r]) * int(pt["pre_tok_ns"]) for r in range(n)]
@@ -152,8 +162,11 @@ def simulate(pt: Dict, arrival, prompt, out, pred, cls) -> Dict[str, np.ndarray]
             k = int(prompt[r]) + int(pred[r])
             inv = F(1.0) / F(pt["kv_cap_dec"])
             fp = lambda x: int(prompt[x]) + int(out[x])
+        offered = range(n_inst)
+        if pt["policy"] == "learned_sampled":
+            offered = sorted(set(_pair(words[r][2 * pool], words[r][2 * pool + 1], n_inst)))
         best, best_key = 0, None
-        for j in range(n_inst):
+        for j in offered:
             kv = sum(fp(x) for x in led[j])
             c = _cost(pt, backlog(pool, j, now, proj), work, sg, kv, k, inv, len(led[j]))
             kk = _key(c)

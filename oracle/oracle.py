@@ -17,7 +17,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("RT_ORACLE_LIB") or os.path.join(HERE, "librt_oracle.so")
 MAX_CLASSES = 8
-POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2}
+POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2, "learned_sampled": 3}
 BACKLOG = {"true": 0, "proxy": 1}
 POOL = {"prefill": 0, "decode": 1}
 
@@ -56,9 +56,11 @@ def lib():
         L = C.CDLL(LIB_PATH)
         P = C.c_void_p
         L.orc_score.argtypes = [C.POINTER(Router), C.c_int32, C.c_int32, P, P, P, C.c_int64, C.c_int64,
-                                C.c_int64, P, P, P, P, P, P]
+                                C.c_int64, P, P, P, P, P, P, P]
         L.orc_score.restype = C.c_int
-        L.orc_sim_replica.argtypes = [C.POINTER(Point), C.c_int64, P, P, P, P, P, P, P, C.c_double,
+        L.orc_candidates.argtypes = [C.c_uint32, C.c_uint32, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_int32)]
+        L.orc_candidates.restype = None
+        L.orc_sim_replica.argtypes = [C.POINTER(Point), C.c_int64, P, P, P, P, P, P, P, P, C.c_double,
                                       P, P, P, P, C.POINTER(Stats)]
         L.orc_sim_replica.restype = C.c_int
         L.orc_goodput.argtypes = [C.POINTER(Point), C.c_int64, P, P, P, P, C.POINTER(C.c_double)]
@@ -95,9 +97,18 @@ def point_struct(d: Dict) -> Point:
     return p
 
 
+def candidates(u: int, v: int, n: int):
+    """The two sampled candidates of a pool of n instances for words u, v."""
+    c1, c2 = C.c_int32(), C.c_int32()
+    lib().orc_candidates(int(u) & 0xFFFFFFFF, int(v) & 0xFFFFFFFF, int(n), C.byref(c1), C.byref(c2))
+    return c1.value, c2.value
+
+
 def score(router: Dict, pool: str, backlog_s, queue, kv_occ, kv_cap: int, n_inst: int, inst_stride: int,
-          prompt_len, pred_out_len, slo_class):
-    """Standalone scorer: (idx i32, score f32, second-best f32) per request."""
+          prompt_len, pred_out_len, slo_class, sample_bits=None):
+    """Standalone scorer: (idx i32, score f32, second-best f32) per request.
+    ``sample_bits`` ([n, 2] uint32, optional) restricts each request to its
+    two sampled candidates."""
     b = np.ascontiguousarray(backlog_s, np.float32)
     q = np.ascontiguousarray(queue, np.int32)
     k = np.ascontiguousarray(kv_occ, np.int32)
@@ -109,16 +120,18 @@ def score(router: Dict, pool: str, backlog_s, queue, kv_occ, kv_cap: int, n_inst
     sc = np.empty(n, np.float32)
     sec = np.empty(n, np.float32)
     r = router_struct(router)
+    sb = None if sample_bits is None else np.ascontiguousarray(sample_bits, np.uint32).reshape(n, 2)
     rc = lib().orc_score(C.byref(r), POOL[pool], n_inst, _ptr(b), _ptr(q), _ptr(k), kv_cap, inst_stride, n,
-                         _ptr(p), _ptr(oh), _ptr(c), _ptr(idx), _ptr(sc), _ptr(sec))
+                         _ptr(p), _ptr(oh), _ptr(c), _ptr(sb), _ptr(idx), _ptr(sc), _ptr(sec))
     if rc != 0:
         raise ValueError(f"orc_score rejected its arguments (rc={rc})")
     return idx, sc, sec
 
 
 def sim_replica(point: Dict, arrival_ns, prompt_len, out_len, pred_out_len, slo_class,
-                follow_pre=None, follow_dec=None, tie_rel: float = 1e-6):
-    """One replica; returns (dict of outputs, dict of stats)."""
+                follow_pre=None, follow_dec=None, tie_rel: float = 1e-6, sample_bits=None):
+    """One replica; returns (dict of outputs, dict of stats).  ``sample_bits``
+    ([n, 4] uint32) is required for the sampled policy."""
     a = np.ascontiguousarray(arrival_ns, np.int64)
     n = a.size
     arrs = [np.ascontiguousarray(x, t) for x, t in ((prompt_len, np.int32), (out_len, np.int32),
@@ -127,9 +140,10 @@ def sim_replica(point: Dict, arrival_ns, prompt_len, out_len, pred_out_len, slo_
     fd = None if follow_dec is None else np.ascontiguousarray(follow_dec, np.int32)
     out = dict(i_pre=np.empty(n, np.int32), i_dec=np.empty(n, np.int32),
                ttft_ns=np.empty(n, np.int64), decode_span_ns=np.empty(n, np.int64))
+    sb = None if sample_bits is None else np.ascontiguousarray(sample_bits, np.uint32).reshape(n, 4)
     st = Stats()
     pst = point_struct(point)
-    rc = lib().orc_sim_replica(C.byref(pst), n, _ptr(a), *[_ptr(x) for x in arrs], _ptr(fp), _ptr(fd),
+    rc = lib().orc_sim_replica(C.byref(pst), n, _ptr(a), *[_ptr(x) for x in arrs], _ptr(sb), _ptr(fp), _ptr(fd),
                                float(tie_rel), _ptr(out["i_pre"]), _ptr(out["i_dec"]), _ptr(out["ttft_ns"]),
                                _ptr(out["decode_span_ns"]), C.byref(st))
     if rc != 0:
@@ -168,8 +182,10 @@ def sim_trace(points: Sequence[Dict], trace: Dict[str, np.ndarray], replicas: Op
         sl = slice(lo, hi)
         fpre = None if follow is None else follow["i_pre"][sl]
         fdec = None if follow is None else follow["i_dec"][sl]
+        sb = trace.get("sample_bits")
         out, st = sim_replica(pt, trace["arrival_ns"][sl], trace["prompt_len"][sl], trace["out_len"][sl],
-                              trace["pred_out_len"][sl], trace["slo_class"][sl], fpre, fdec, tie_rel)
+                              trace["pred_out_len"][sl], trace["slo_class"][sl], fpre, fdec, tie_rel,
+                              None if sb is None else sb[sl])
         g, met = goodput(pt, trace["out_len"][sl], trace["slo_class"][sl], out["ttft_ns"], out["decode_span_ns"])
         return i, (out, st, g, met)
 

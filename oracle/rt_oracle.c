@@ -52,10 +52,23 @@ static int64_t pool_need(int32_t pool, int32_t p, int32_t ohat) {
   return pool == ORC_PREFILL ? (int64_t)p : (int64_t)p + (int64_t)ohat;
 }
 
+void orc_candidates(uint32_t u, uint32_t v, int32_t n, int32_t* c1, int32_t* c2) {
+  const uint64_t first = ((uint64_t)u * (uint64_t)n) >> 32;
+  *c1 = (int32_t)first;
+  if (n < 2) {
+    *c2 = *c1;
+    return;
+  }
+  /* the v-th of the n - 1 instances other than the first, in index order */
+  const uint64_t k = ((uint64_t)v * (uint64_t)(n - 1)) >> 32;
+  *c2 = (int32_t)(k < first ? k : k + 1);
+}
+
 int orc_score(const orc_router* rp, int32_t pool, int32_t n_inst, const float* backlog_s,
               const int32_t* queue, const int32_t* kv_occ, int64_t kv_cap, int64_t inst_stride,
               int64_t n_req, const int32_t* prompt_len, const int32_t* pred_out_len,
-              const uint8_t* slo_class, int32_t* out_idx, float* out_score, float* out_second) {
+              const uint8_t* slo_class, const uint32_t* sample_bits, int32_t* out_idx, float* out_score,
+              float* out_second) {
   if (!rp || n_inst < 1 || n_req < 0 || kv_cap < 1 || (pool != ORC_PREFILL && pool != ORC_DECODE))
     return -1;
   if (n_req > 0 && (!backlog_s || !queue || !kv_occ || !prompt_len || !pred_out_len || !slo_class ||
@@ -79,7 +92,10 @@ int orc_score(const orc_router* rp, int32_t pool, int32_t n_inst, const float* b
     const int64_t row = i * inst_stride;
     int32_t best = -1;
     float best_c = 0.0f, second_c = INFINITY;
+    int32_t c1 = -1, c2 = -1;
+    if (sample_bits) orc_candidates(sample_bits[2 * i], sample_bits[2 * i + 1], n_inst, &c1, &c2);
     for (int32_t j = 0; j < n_inst; ++j) {
+      if (sample_bits && j != c1 && j != c2) continue; /* not offered */
       float c_j = cost_eq(rp, backlog_s[row + j], work, sg, kv_occ[row + j], k, inv_cap, queue[row + j]);
       if (best < 0 || cost_key(c_j) < cost_key(best_c)) {
         if (best >= 0) second_c = best_c;
@@ -175,13 +191,16 @@ static float backlog_of(const orc_point* pt, int32_t pool, const inst_t* s, int6
   return rp->tau_dec_s * (float)s->pend;
 }
 
-/* Own choice for one pool.  Returns the argmin; fills cost[] (learned only)
- * and reports whether the best two costs are within tie_rel. */
+/* Own choice for one pool.  Returns the argmin over the offered instances
+ * (every instance, or under the sampled policy the two candidates drawn from
+ * `words`, returned in cand[]); fills cost[] (learned policies only) and
+ * reports whether the best two offered costs are within tie_rel. */
 static int32_t choose(const orc_point* pt, int32_t pool, const inst_t* inst, int32_t n, int64_t r,
-                      int64_t now, int32_t p, int32_t ohat, uint8_t c, double tie_rel, float* cost,
-                      int* tie, int* close) {
+                      int64_t now, int32_t p, int32_t ohat, uint8_t c, const uint32_t* words, double tie_rel,
+                      float* cost, int32_t* cand, int* tie, int* close) {
   *tie = 0;
   *close = 0;
+  cand[0] = cand[1] = -1;
   if (pt->policy == ORC_ROUND_ROBIN) return (int32_t)(r % n);
   if (pt->policy == ORC_LEAST_LOADED) {
     int32_t b = 0;
@@ -195,12 +214,16 @@ static int32_t choose(const orc_point* pt, int32_t pool, const inst_t* inst, int
   const int64_t k = pool_need(pool, p, ohat);
   const int64_t cap = pool == ORC_PREFILL ? pt->kv_cap_pre : pt->kv_cap_dec;
   const float inv_cap = 1.0f / (float)cap;
-  int32_t b = 0, b2 = -1;
+  const int sampled = pt->policy == ORC_LEARNED_SAMPLED;
+  if (sampled) orc_candidates(words[0], words[1], n, &cand[0], &cand[1]);
+  int32_t b = -1, b2 = -1;
   for (int32_t j = 0; j < n; ++j) {
     cost[j] = cost_eq(rp, backlog_of(pt, pool, &inst[j], now), work, sg, inst[j].kv, k, inv_cap,
                       inst[j].queue);
-    if (j == 0) continue;
-    if (cost_key(cost[j]) < cost_key(cost[b])) {
+    if (sampled && j != cand[0] && j != cand[1]) continue; /* not offered */
+    if (b < 0) {
+      b = j;
+    } else if (cost_key(cost[j]) < cost_key(cost[b])) {
       b2 = b;
       b = j;
     } else if (b2 < 0 || cost_key(cost[j]) < cost_key(cost[b2])) {
@@ -218,10 +241,12 @@ static int32_t choose(const orc_point* pt, int32_t pool, const inst_t* inst, int
 
 /* Adopt an external placement g in place of the own choice m. */
 static int32_t follow(const orc_point* pt, int32_t m, int32_t g, int32_t n, const float* cost,
-                      double tie_rel, int64_t* near_tie, int64_t* mismatch, int64_t* first, int64_t r) {
+                      const int32_t* cand, double tie_rel, int64_t* near_tie, int64_t* mismatch, int64_t* first,
+                      int64_t r) {
   if (g == m) return m;
   int ok = 0;
-  if (g >= 0 && g < n && pt->policy == ORC_LEARNED) {
+  const int offered = pt->policy == ORC_LEARNED || (pt->policy == ORC_LEARNED_SAMPLED && (g == cand[0] || g == cand[1]));
+  if (g >= 0 && g < n && offered) {
     double gap = (double)cost[g] - (double)cost[m];
     ok = gap <= tie_rel * fabs((double)cost[m]);
   }
@@ -236,7 +261,7 @@ static int32_t follow(const orc_point* pt, int32_t m, int32_t g, int32_t n, cons
 
 int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
                     const int32_t* prompt_len, const int32_t* out_len,
-                    const int32_t* pred_out_len, const uint8_t* slo_class,
+                    const int32_t* pred_out_len, const uint8_t* slo_class, const uint32_t* sample_bits,
                     const int32_t* follow_pre, const int32_t* follow_dec, double tie_rel,
                     int32_t* i_pre, int32_t* i_dec, int64_t* ttft_ns, int64_t* span_ns,
                     orc_stats* st) {
@@ -247,6 +272,7 @@ int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
   if (n > 0 && (!arrival_ns || !prompt_len || !out_len || !pred_out_len || !slo_class || !i_pre ||
                 !i_dec || !ttft_ns || !span_ns))
     return -1;
+  if (pt->policy == ORC_LEARNED_SAMPLED && n > 0 && !sample_bits) return -1;
   memset(st, 0, sizeof *st);
   st->first_mismatch = -1;
   const int32_t P = pt->n_prefill, D = pt->n_decode;
@@ -283,17 +309,20 @@ int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
 
     /* 2. argmin of each pool, computed independently on the same state. */
     int tie, close;
-    int32_t ip = choose(pt, ORC_PREFILL, pre, P, r, now, p, oh, c, tie_rel, cost_pre, &tie, &close);
+    int32_t cand_pre[2], cand_dec[2];
+    const uint32_t* w = sample_bits ? sample_bits + 4 * r : NULL;
+    int32_t ip = choose(pt, ORC_PREFILL, pre, P, r, now, p, oh, c, w, tie_rel, cost_pre, cand_pre, &tie, &close);
     st->tie_pre += tie;
     st->close_pre += close;
-    int32_t id = choose(pt, ORC_DECODE, dec, D, r, now, p, oh, c, tie_rel, cost_dec, &tie, &close);
+    int32_t id = choose(pt, ORC_DECODE, dec, D, r, now, p, oh, c, w ? w + 2 : NULL, tie_rel, cost_dec, cand_dec,
+                        &tie, &close);
     st->tie_dec += tie;
     st->close_dec += close;
     if (follow_pre)
-      ip = follow(pt, ip, follow_pre[r], P, cost_pre, tie_rel, &st->near_tie_pre, &st->mismatch_pre,
+      ip = follow(pt, ip, follow_pre[r], P, cost_pre, cand_pre, tie_rel, &st->near_tie_pre, &st->mismatch_pre,
                   &st->first_mismatch, r);
     if (follow_dec)
-      id = follow(pt, id, follow_dec[r], D, cost_dec, tie_rel, &st->near_tie_dec, &st->mismatch_dec,
+      id = follow(pt, id, follow_dec[r], D, cost_dec, cand_dec, tie_rel, &st->near_tie_dec, &st->mismatch_dec,
                   &st->first_mismatch, r);
 
     /* 3. prefill on ip, transfer the KV, decode on id: one request at a time

@@ -37,7 +37,10 @@ extern "C" {
 
 #define ORC_MAX_CLASSES 8
 
-enum { ORC_LEARNED = 0, ORC_ROUND_ROBIN = 1, ORC_LEAST_LOADED = 2 };
+/* ORC_LEARNED_SAMPLED: the learned score over two random candidates per pool
+ * (the sampled variant Section V-E and Section VI name as the mitigation for
+ * scarce pools).  The random words are inputs (see orc_candidates). */
+enum { ORC_LEARNED = 0, ORC_ROUND_ROBIN = 1, ORC_LEAST_LOADED = 2, ORC_LEARNED_SAMPLED = 3 };
 enum { ORC_BACKLOG_TRUE = 0, ORC_BACKLOG_PROXY = 1 };
 enum { ORC_PREFILL = 0, ORC_DECODE = 1 };
 
@@ -73,11 +76,22 @@ typedef struct {
   int64_t end_inflight_pre, end_inflight_dec; /* after the last arrival       */
 } orc_stats;
 
+/* The two candidates a pool of n >= 1 instances offers for one request,
+ * from the request's two random words u, v of that pool: the first is
+ * floor(u * n / 2^32); the second is drawn the same way from v among the
+ * n - 1 others (floor(v * (n - 1) / 2^32), counted past the first), so that
+ * the two differ whenever n >= 2; with n == 1 both are instance 0. */
+void orc_candidates(uint32_t u, uint32_t v, int32_t n, int32_t* c1, int32_t* c2);
+
 /* Score n_inst instances of one pool for each of n_req requests.
  *   backlog_s/queue/kv_occ: instance snapshot; request i uses row
  *   i*inst_stride (inst_stride 0 = one snapshot shared by all requests).
  *   out_idx[i] = argmin (lowest index on equal cost), out_score[i] = its cost;
  *   out_second[i] (may be NULL) = second-lowest cost (+inf if n_inst == 1).
+ *   sample_bits (may be NULL): [n_req][2] words u, v; when given, only the
+ *   two candidates orc_candidates draws from them are scored, out_idx is the
+ *   cheaper of the two (lower index on equal cost) and out_second the other
+ *   one's cost (+inf if n_inst == 1).
  *   A request with prompt_len < 1, slo_class >= ORC_MAX_CLASSES or (decode
  *   pool) pred_out_len < 1 or prompt_len + pred_out_len >= 2^31 gets idx -1
  *   and NaN scores.
@@ -85,12 +99,16 @@ typedef struct {
 int orc_score(const orc_router* rp, int32_t pool, int32_t n_inst, const float* backlog_s,
               const int32_t* queue, const int32_t* kv_occ, int64_t kv_cap, int64_t inst_stride,
               int64_t n_req, const int32_t* prompt_len, const int32_t* pred_out_len,
-              const uint8_t* slo_class, int32_t* out_idx, float* out_score, float* out_second);
+              const uint8_t* slo_class, const uint32_t* sample_bits, int32_t* out_idx, float* out_score,
+              float* out_second);
 
 /* Simulate one replica of n requests (arrays indexed 0..n-1).
  *   follow_pre/follow_dec: NULL for a free run, else externally chosen
  *   placements to adopt (see the header comment); tie_rel is the relative
- *   tolerance under which a divergent learned placement is accepted.
+ *   tolerance under which a divergent learned placement is accepted (under
+ *   the sampled policy only a placement on one of the two candidates).
+ *   sample_bits: [n][4] words for ORC_LEARNED_SAMPLED (words 0, 1 draw the
+ *   prefill candidates, words 2, 3 the decode ones); NULL otherwise.
  *   Outputs: i_pre, i_dec, ttft_ns = prefill end - arrival,
  *   span_ns = decode end - prefill end; all -1 for a rejected request (a
  *   length < 1, a token total p + o or p + o^ >= 2^31, a class out of range,
@@ -98,7 +116,7 @@ int orc_score(const orc_router* rp, int32_t pool, int32_t n_inst, const float* b
  * Returns 0, -1 on a bad argument, -2 on allocation failure. */
 int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
                     const int32_t* prompt_len, const int32_t* out_len,
-                    const int32_t* pred_out_len, const uint8_t* slo_class,
+                    const int32_t* pred_out_len, const uint8_t* slo_class, const uint32_t* sample_bits,
                     const int32_t* follow_pre, const int32_t* follow_dec, double tie_rel,
                     int32_t* i_pre, int32_t* i_dec, int64_t* ttft_ns, int64_t* span_ns,
                     orc_stats* st);

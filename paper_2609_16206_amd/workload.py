@@ -356,6 +356,23 @@ def replica_arrays(seed: int, replica: int, traffic: Traffic, n: int) -> Dict[st
     return dict(arrival_ns=arr, prompt_len=p, out_len=o, pred_out_len=oh, slo_class=cls)
 
 
+def sample_words(seed: int, replica: int, n: int) -> np.ndarray:
+    """[n, 4] uint32 random words of one replica for the sampled policy (two
+    per pool), from a stream of their own so that the other arrays do not
+    depend on whether they are drawn."""
+    rng = np.random.default_rng([int(seed), int(replica), 1])
+    return rng.integers(0, 1 << 32, size=(n, 4), dtype=np.uint32)
+
+
+def add_sample_words(trace: Dict[str, np.ndarray], seed: int, replicas: Optional[Sequence[int]] = None) -> None:
+    """Attach ``sample_bits`` ([n_requests, 4] uint32) to an SoA trace: the
+    words of trace replica k are those of workload replica replicas[k]."""
+    off = trace["offsets"]
+    reps = range(len(off) - 1) if replicas is None else replicas
+    parts = [sample_words(seed, int(r), int(off[k + 1] - off[k])) for k, r in enumerate(reps)]
+    trace["sample_bits"] = np.concatenate(parts) if parts else np.zeros((0, 4), np.uint32)
+
+
 # --------------------------------------------------------------------------
 # Workloads
 # --------------------------------------------------------------------------
@@ -420,6 +437,8 @@ def make_trace(wl: Workload, replicas: Optional[Sequence[int]] = None, workers: 
                        slo_class=np.zeros(0, np.uint8))
     out["offsets"] = np.arange(reps.size + 1, dtype=np.int64) * n
     out["param_point"] = pts_all
+    if any(p["policy"] == "learned_sampled" for p in wl.points):
+        add_sample_words(out, wl.seed, reps)
     return out
 
 

@@ -39,7 +39,9 @@ def follow_replicas(points, trace: Dict[str, np.ndarray], gpu: Dict[str, np.ndar
         sl = slice(lo, hi)
         pt = points[int(pp[i])]
         args = [trace[k][sl] for k in KEYS]
-        out, st = O.sim_replica(pt, *args, follow_pre=gpu["i_pre"][sl], follow_dec=gpu["i_dec"][sl], tie_rel=TIE_REL)
+        sb = trace["sample_bits"][sl] if "sample_bits" in trace else None
+        out, st = O.sim_replica(pt, *args, follow_pre=gpu["i_pre"][sl], follow_dec=gpu["i_dec"][sl], tie_rel=TIE_REL,
+                                sample_bits=sb)
         res = dict(rep=i, n=hi - lo, near_tie=st["near_tie_pre"] + st["near_tie_dec"],
                    mismatch=st["mismatch_pre"] + st["mismatch_dec"], first=st["first_mismatch"],
                    close=st["close_pre"] + st["close_dec"], invalid=st["invalid"])

@@ -167,8 +167,8 @@ def test_event_heap_bruteforce_agrees():
     for case in range(2000):
         P, D = (int(x) for x in rng.integers(1, 4, size=2))
         n = int(rng.integers(1, 17))
-        pol = ("learned", "round_robin", "least_loaded")[case % 3]
-        mode = ("true", "proxy")[(case // 3) % 2]
+        pol = ("learned", "round_robin", "least_loaded", "learned_sampled")[case % 4]
+        mode = ("true", "proxy")[(case // 4) % 2]
         pt = W.make_point(P, D, n_classes=3, policy=pol, backlog_mode=mode,
                           physics=dict(pre_base_ns=int(rng.integers(0, 3)) * 10,
                                        pre_tok_ns=int(rng.integers(0, 3)) * 10,
@@ -181,8 +181,9 @@ def test_event_heap_bruteforce_agrees():
         o = rng.integers(1, 5, n).astype(np.int32)
         oh = rng.integers(1, 5, n).astype(np.int32)
         c = rng.integers(0, 3, n).astype(np.uint8)
-        ref = H.simulate(pt, arr, p, o, oh, c)
-        got, st = O.sim_replica(pt, arr, p, o, oh, c)
+        words = rng.integers(0, 1 << 32, size=(n, 4), dtype=np.uint64).astype(np.uint32)
+        ref = H.simulate(pt, arr, p, o, oh, c, words)
+        got, st = O.sim_replica(pt, arr, p, o, oh, c, sample_bits=words)
         for k in ref:
             assert np.array_equal(ref[k], got[k]), (case, k, ref[k], got[k])
         assert st["violations"] == 0
