@@ -30,6 +30,7 @@ HBM_PEAK = 8.0e12  # B/s, MI355X HBM3E
 ALU_PEAK = 256 * 4 * 16 * 2.4e9
 # Algorithmic work per unit (derivation in the design notes):
 SIM_BYTES_PER_REQ = 21 + 24  # trace in (i64 + 3 x i32 + u8), outputs out (2 x i32 + 2 x i64)
+SAMPLE_BYTES_PER_REQ = 16  # the sampled policy's four candidate words
 SIM_OPS_PER_PAIR = 19  # backlog 4, press 3, (1 + rho press) 2, size 2, load 2, queue 2, sums 2, argmin 1, release 1
 SIM_OPS_PER_REQ = 25  # priced work, need, service times, Lindley updates, state and outputs
 SCORE_BYTES_PER_REQ = 4 + 4 + 1 + 4 + 4  # p, o^, class in; index, score out
@@ -43,6 +44,8 @@ def _workload(name):
         return W.tiny_sim()
     if name == "cluster":
         return W.paper_cluster()
+    if name == "cluster_sampled":
+        return W.paper_cluster(policy="learned_sampled")
     if name == "sweep":
         return W.param_sweep()
     if name == "large":
@@ -59,7 +62,7 @@ def _source_hash(files):
 
 
 SIM_SOURCES = ["paper_2609_16206_amd/csrc/" + f for f in (
-    "seg_kernel.h", "wseg_kernel.h", "seg_true.hip", "seg_proxy.hip", "seg_base.hip", "seg_classes.hip",
+    "seg_kernel.h", "wseg_kernel.h", "seg_true.hip", "seg_proxy.hip", "seg_base.hip", "seg_true_s.hip", "seg_proxy_s.hip", "seg_classes.hip",
     "lane_ops.h", "rt_internal.h")]
 SCORE_SOURCES = ["paper_2609_16206_amd/csrc/score_kernel.hip", "paper_2609_16206_amd/csrc/rt_internal.h"]
 
@@ -149,7 +152,7 @@ def bench_sim(args):
     ms_step = dt * 1e3 / args.steps
     value = n_req * args.steps / dt
     kernel_s = kern_ms * 1e-3 / max(1, calls)
-    alg_bytes = n_req * SIM_BYTES_PER_REQ
+    alg_bytes = n_req * (SIM_BYTES_PER_REQ + (SAMPLE_BYTES_PER_REQ if "sample_bits" in tr else 0))
     alg_ops = n_pairs * SIM_OPS_PER_PAIR + n_req * SIM_OPS_PER_REQ
     t_hbm, t_alu = alg_bytes / HBM_PEAK, alg_ops / ALU_PEAK
     if t_hbm >= t_alu:
@@ -240,7 +243,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="cluster", choices=["tiny", "cluster", "sweep", "large", "scorer"])
+    ap.add_argument("--workload", default="cluster",
+                    choices=["tiny", "cluster", "cluster_sampled", "sweep", "large", "scorer"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",

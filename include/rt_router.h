@@ -65,7 +65,11 @@ typedef enum {
 typedef enum {
   RT_POLICY_LEARNED = 0,      /* the marginal-cost scorer (Section III-A)              */
   RT_POLICY_ROUND_ROBIN = 1,  /* request r goes to instance r mod N (Section IV-C)     */
-  RT_POLICY_LEAST_LOADED = 2  /* fewest in-flight requests, lowest index on ties       */
+  RT_POLICY_LEAST_LOADED = 2, /* fewest in-flight requests, lowest index on ties       */
+  RT_POLICY_LEARNED_SAMPLED = 3 /* the scorer over two random candidates per pool: the
+                                   sampled variant that Section V-E and Section VI give
+                                   as the mitigation for scarce pools (candidates: see
+                                   rt_sim_run_replicas)                                */
 } rt_policy;
 
 typedef enum {
@@ -136,6 +140,10 @@ typedef struct {
                                   never reads it                                          */
   const int32_t* pred_out_len; /* o^_r >= 1, predicted output length                      */
   const uint8_t* slo_class;    /* s_r < the point's n_classes                             */
+  const uint32_t* sample_bits; /* [n_requests][4] random words for RT_POLICY_LEARNED_SAMPLED:
+                                  words 0, 1 draw request r's prefill candidates, words
+                                  2, 3 its decode candidates; required when a replica
+                                  uses that policy, else may be NULL (never read)         */
 } rt_trace;
 
 /* Per-request outputs, device memory, each of length trace->n_requests
@@ -159,10 +167,17 @@ typedef struct {
  * bit set) if p_r, o_r or o^_r < 1, p_r + o_r or p_r + o^_r >= 2^31, its class
  * is out of range, or its arrival is negative or earlier than the replica's
  * previous accepted arrival.
+ * Under RT_POLICY_LEARNED_SAMPLED a pool of n instances offers two candidates
+ * drawn from the request's two words u, v of that pool:
+ *   c1 = floor(u * n / 2^32);  n == 1: c2 = c1;  else with
+ *   x = floor(v * (n - 1) / 2^32), c2 = x + (x >= c1 ? 1 : 0)
+ * (two distinct instances, every ordered pair equally likely up to a bias of
+ * n / 2^32), and the request goes to the cheaper of the two, the lower index
+ * on equal cost.  With n <= 2 this is the full argmin.
  * The call reads offsets and param_point back to the host to plan the launch
  * (it synchronizes `hip_stream` for that), validates them (RT_EINVAL), then
  * enqueues the simulation on `hip_stream` and returns.  Scratch memory grows
- * with n_requests (40 bytes per request) and is owned by `sim`. */
+ * with n_requests (80 bytes per request) and is owned by `sim`. */
 rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* out, void* hip_stream);
 
 /* Per-replica goodput: the fraction of the replica's requests that meet both

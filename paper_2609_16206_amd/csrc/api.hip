@@ -49,7 +49,7 @@ std::string check_point(const rt_point& p) {
   if (p.n_prefill < 1 || p.n_decode < 1) return "pool sizes must be >= 1";
   if (p.n_prefill > RT_MAX_POOL || p.n_decode > RT_MAX_POOL) return "pool wider than RT_MAX_POOL";
   if (p.n_classes < 1 || p.n_classes > RT_MAX_CLASSES) return "n_classes must be in [1, RT_MAX_CLASSES]";
-  if (p.policy < RT_POLICY_LEARNED || p.policy > RT_POLICY_LEAST_LOADED) return "unknown policy";
+  if (p.policy < RT_POLICY_LEARNED || p.policy > RT_POLICY_LEARNED_SAMPLED) return "unknown policy";
   if (p.backlog_mode != RT_BACKLOG_TRUE && p.backlog_mode != RT_BACKLOG_PROXY) return "unknown backlog_mode";
   const rt_router_params& r = p.router;
   const float f[] = {r.w_b, r.w_s, r.w_q, r.rho, r.tau_pre_s, r.tau_dec_s, r.pre_base_s};
@@ -104,8 +104,10 @@ rt::DevPoint to_dev(const rt_point& p) {
 
 // The scoring path a point's kernels take.
 int point_mode(const rt_point& p) {
-  if (p.policy != RT_POLICY_LEARNED) return rt::kModeBase;
-  return p.backlog_mode == RT_BACKLOG_TRUE ? rt::kModeTrue : rt::kModeProxy;
+  const bool tr = p.backlog_mode == RT_BACKLOG_TRUE;
+  if (p.policy == RT_POLICY_LEARNED) return tr ? rt::kModeTrue : rt::kModeProxy;
+  if (p.policy == RT_POLICY_LEARNED_SAMPLED) return tr ? rt::kModeTrueSampled : rt::kModeProxySampled;
+  return rt::kModeBase;
 }
 
 // Does kernel class c hold both pools of point p?  A one-wave segment class
@@ -316,6 +318,10 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   std::vector<int64_t> reps_of(npts, 0);
   for (int64_t i = 0; i < n; ++i)
     if (off[i + 1] > off[i]) reps_of[pp[i]] += 1;
+  for (size_t k = 0; k < npts; ++k)
+    if (reps_of[k] > 0 && sim->points[k].policy == RT_POLICY_LEARNED_SAMPLED && !trace->sample_bits)
+      return fail(RT_EINVAL, "rt_sim_run_replicas: point " + std::to_string(k) +
+                                 " samples candidates but trace->sample_bits is NULL");
   double waves = 0.0;
   for (size_t k = 0; k < npts; ++k) waves += (double)reps_of[k] * rt::sim_class(sim->point_classes[k][0]).S / 64.0;
   const bool many = waves >= 2.0 * kSimds;
@@ -403,6 +409,7 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   a.olen = trace->out_len;
   a.ohat = trace->pred_out_len;
   a.cls = trace->slo_class;
+  a.samp = trace->sample_bits;
   a.i_pre = out->i_pre;
   a.i_dec = out->i_dec;
   a.ttft = out->ttft_ns;

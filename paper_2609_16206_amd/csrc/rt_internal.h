@@ -25,7 +25,7 @@ struct DevPoint {
 enum : uint32_t { kFlagRejected = 1u, kFlagBadTrace = 2u, kFlagTimeRange = 4u };
 
 // rt_policy values as the kernels read them from DevPoint::policy.
-enum : int32_t { kPolicyLearned = 0, kPolicyRoundRobin = 1, kPolicyLeastLoaded = 2 };
+enum : int32_t { kPolicyLearned = 0, kPolicyRoundRobin = 1, kPolicyLeastLoaded = 2, kPolicyLearnedSampled = 3 };
 
 // Arguments of the replica-simulation kernels.
 struct SimArgs {
@@ -39,6 +39,7 @@ struct SimArgs {
   const int32_t* olen;
   const int32_t* ohat;
   const uint8_t* cls;
+  const uint32_t* samp;  // [n][4] candidate words (sampled modes only)
   int32_t* i_pre;
   int32_t* i_dec;
   int64_t* ttft;
@@ -67,11 +68,13 @@ constexpr int kDummyRecords = 1024;  // a power of two
 // Kernel classes.  kSeg: one replica per aligned segment of S <= 64 lanes of
 // one wave, prefill instances on the first lanes and decode instances on the
 // next, MP = MD instances per lane; `mode` fixes the scoring path (clock
-// backlog, ledger backlog, or a baseline policy).  kWseg: the same for one
-// replica per workgroup of S / 64 waves, instances dealt round-robin over the
-// waves.
+// backlog, ledger backlog, or a baseline policy; the two learned ones also
+// over two sampled candidates per pool).  kWseg: the same for one replica
+// per workgroup of S / 64 waves, instances dealt round-robin over the waves.
 enum SimKind { kSeg = 0, kWseg = 1 };
-enum SimMode { kModeTrue = 0, kModeProxy = 1, kModeBase = 2 };
+enum SimMode { kModeTrue = 0, kModeProxy = 1, kModeBase = 2, kModeTrueSampled = 3, kModeProxySampled = 4 };
+constexpr bool mode_ledger(int m) { return m == kModeProxy || m == kModeProxySampled; }  // proxy backlog
+constexpr bool mode_sampled(int m) { return m == kModeTrueSampled || m == kModeProxySampled; }
 
 struct SimClass {
   int kind, S, MP, MD, mode;

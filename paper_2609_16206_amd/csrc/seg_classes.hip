@@ -22,18 +22,19 @@ constexpr int kNumShapes = (int)(sizeof(kShapes) / sizeof(kShapes[0]));
 const SegShape kWideShapes[] = {RT_WSEG_FOR_EACH(RT_WSEG_SHAPE)};
 #undef RT_WSEG_SHAPE
 constexpr int kNumWide = (int)(sizeof(kWideShapes) / sizeof(kWideShapes[0]));
-constexpr int kModes[] = {kModeTrue, kModeProxy, kModeBase};
+constexpr int kModes[] = {kModeTrue, kModeProxy, kModeBase, kModeTrueSampled, kModeProxySampled};
+constexpr int kNumModes = (int)(sizeof(kModes) / sizeof(kModes[0]));
 
 }  // namespace
 
-int sim_class_count() { return (kNumShapes + kNumWide) * 3; }
+int sim_class_count() { return (kNumShapes + kNumWide) * kNumModes; }
 
 SimClass sim_class(int i) {
-  if (i < kNumShapes * 3) {
+  if (i < kNumShapes * kNumModes) {
     const SegShape& e = kShapes[i % kNumShapes];
     return SimClass{kSeg, e.S, e.M, e.M, kModes[i / kNumShapes]};
   }
-  i -= kNumShapes * 3;
+  i -= kNumShapes * kNumModes;
   const SegShape& e = kWideShapes[i % kNumWide];
   return SimClass{kWseg, 64 * e.S, e.M, e.M, kModes[i / kNumWide]};
 }
@@ -49,6 +50,12 @@ hipError_t launch_sim(const SimClass& c, const SimArgs& a, hipStream_t stream) {
                : seg::launch_mode<kModeProxy>(S, c.MP, a, stream);
     case kModeBase:
       return w ? seg::launch_wide_mode<kModeBase>(S, c.MP, a, stream) : seg::launch_mode<kModeBase>(S, c.MP, a, stream);
+    case kModeTrueSampled:
+      return w ? seg::launch_wide_mode<kModeTrueSampled>(S, c.MP, a, stream)
+               : seg::launch_mode<kModeTrueSampled>(S, c.MP, a, stream);
+    case kModeProxySampled:
+      return w ? seg::launch_wide_mode<kModeProxySampled>(S, c.MP, a, stream)
+               : seg::launch_mode<kModeProxySampled>(S, c.MP, a, stream);
     default:
       return hipErrorInvalidValue;
   }

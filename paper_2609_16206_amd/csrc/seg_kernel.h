@@ -175,6 +175,15 @@ __device__ __forceinline__ Req admit_check(int32_t rem, int32_t ncls, int64_t ar
   return q;
 }
 
+// The two sampled candidates of a pool of n instances from the request's two
+// words of that pool (the rule rt_sim_run_replicas documents): c1 and c2
+// are distinct when n >= 2; with n == 1 both are instance 0.
+__device__ __forceinline__ void sample_pair(uint32_t u, uint32_t v, uint32_t n, uint32_t& c1, uint32_t& c2) {
+  c1 = __umulhi(u, n);
+  const uint32_t x = __umulhi(v, n - 1);
+  c2 = n > 1 ? x + (x >= c1 ? 1u : 0u) : c1;
+}
+
 // Release: up to two completions per instance from the register window; the
 // new head's successors are loaded unconditionally (the wave's dummy record
 // `dmy` when there is nothing to load) and merged later.
@@ -243,8 +252,9 @@ __device__ __forceinline__ void release_more(bool more, Slot (&s)[M], double now
 
 template <int S, int M, int kMode, int kWaves>
 __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
-  constexpr bool kTok = kMode == kModeProxy;  // the ledger is priced
-  constexpr bool kKv = kMode != kModeBase;    // occupancy is priced
+  constexpr bool kTok = mode_ledger(kMode);     // the ledger is priced
+  constexpr bool kKv = kMode != kModeBase;      // occupancy is priced
+  constexpr bool kSamp = mode_sampled(kMode);   // two candidates per pool
   constexpr int kSegs = 64 / S;               // replicas per wave
   const int lane = threadIdx.x & 63;
   const int sl = lane & (S - 1);
@@ -308,6 +318,7 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     int64_t arr;
     int32_t p, o, oh;
     uint32_t c;
+    uint32_t u, v;  // the lane's pool's candidate words (sampled modes)
   };
   auto load_feat = [&](Feat& f, int32_t tt) {
     const int64_t g = rd_base + min(tt, rd_last);
@@ -316,6 +327,13 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     f.o = a.olen[g];
     f.oh = a.ohat[g];
     f.c = a.cls[g];
+    if constexpr (kSamp) {
+      const uint2 w = *reinterpret_cast<const uint2*>(a.samp + 4 * g + (isp ? 0 : 2));
+      f.u = w.x;
+      f.v = w.y;
+    } else {
+      f.u = f.v = 0;
+    }
   };
 
   int32_t rr = 0;     // round robin: t mod (size of this lane's pool)
@@ -323,6 +341,7 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   uint32_t rej = 0;   // a rejected request was recorded by this lane
   Req cur;            // request t, checked, its releases done
   float sg;           // sigma of request t's class
+  uint32_t cu = 0, cv = 0;  // request t's candidate words (sampled modes)
 
   // Step t: score, argmin, serve and record request t; store; then merge the
   // successors loaded during the releases for request t (a step ago), check
@@ -340,6 +359,8 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     uint32_t bkey = 0xffffffffu;
     int32_t bm = 0;
     double bbusy = s[0].busy;
+    uint32_t c1 = 0, c2 = 0;  // the pool's sampled candidates
+    if constexpr (kSamp) sample_pair(cu, cv, (uint32_t)npool, c1, c2);
 #pragma unroll
     for (int m = 0; m < M; ++m) {
       const Slot& x = s[m];
@@ -348,7 +369,7 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
         key = policy == kPolicyLeastLoaded ? (uint32_t)x.q : ((j0 + m) == rr ? 0u : 1u);
       } else {
         float bl;
-        if constexpr (kMode == kModeTrue)
+        if constexpr (!kTok)
           bl = (float)__builtin_fmax(x.busy - now, 0.0) * 1e-9f;
         else
           bl = tau * (float)x.pend + basec * (float)x.q;
@@ -357,6 +378,10 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
         const float size = work * (1.0f + rho * press) * sg;
         const float cost = load + size + w_q * (float)x.q;
         key = cost != cost ? 0x7fc00000u : __float_as_uint(cost);
+      }
+      if constexpr (kSamp) {
+        const uint32_t j = (uint32_t)(j0 + m);
+        key = (j == c1 || j == c2) ? key : 0xffffffffu;
       }
       key = ok[m] ? key : 0xffffffffu;
       if (m == 0) {
@@ -456,7 +481,10 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
       merge_pending(s[m]);
       pin_window(s[m]);
     }
-    asm volatile("" : "+v"(nx.arr), "+v"(nx.p), "+v"(nx.o), "+v"(nx.oh), "+v"(nx.c));
+    if constexpr (kSamp)
+      asm volatile("" : "+v"(nx.arr), "+v"(nx.p), "+v"(nx.o), "+v"(nx.oh), "+v"(nx.c), "+v"(nx.u), "+v"(nx.v));
+    else
+      asm volatile("" : "+v"(nx.arr), "+v"(nx.p), "+v"(nx.o), "+v"(nx.oh), "+v"(nx.c));
     __builtin_amdgcn_sched_barrier(0);
 
     // 6. request t+1: check, sigma, releases (the test for a slow path is
@@ -464,6 +492,8 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     // wait for its vector compare); load request t+2
     cur = admit_check(R - (t + 1), ncls, nx.arr, nx.p, nx.o, nx.oh, nx.c, last_now);
     sg = sig[segw * kMaxClasses + (nx.c & (kMaxClasses - 1))];
+    cu = nx.u;
+    cv = nx.v;
     const bool more = __any(third_min(s) <= cur.now_eff);
     release_fast<M, kTok, kKv>(s, cur.now_eff, recb, tokb, base, R, dmy);
     release_more<M, kTok, kKv>(more, s, cur.now_eff, recb, tokb, base, R, dmy);
@@ -476,6 +506,8 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   __builtin_amdgcn_s_waitcnt(0);
   cur = admit_check(R, ncls, fa.arr, fa.p, fa.o, fa.oh, fa.c, last_now);
   sg = sig[segw * kMaxClasses + (fa.c & (kMaxClasses - 1))];
+  cu = fa.u;
+  cv = fa.v;
   load_feat(fa, 1);
   // enter the loop with nothing in flight, so that the loop header needs no
   // wait

@@ -39,8 +39,9 @@ __host__ __device__ inline int wide_pool_lanes(int n, int M, int W) { return ((n
 
 template <int W, int M, int kMode>
 __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
-  constexpr bool kTok = kMode == kModeProxy;  // the ledger is priced
-  constexpr bool kKv = kMode != kModeBase;    // occupancy is priced
+  constexpr bool kTok = mode_ledger(kMode);    // the ledger is priced
+  constexpr bool kKv = kMode != kModeBase;     // occupancy is priced
+  constexpr bool kSamp = mode_sampled(kMode);  // two candidates per pool
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int rep = a.work[blockIdx.x];
@@ -88,10 +89,22 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   double last_now = 0.0;
   Req cur = admit_check(R, ncls, a.arrival[base], a.plen[base], a.olen[base], a.ohat[base], a.cls[base], last_now);
   float sg = sig[a.cls[base] & (kMaxClasses - 1)];
+  // the candidate words of the lane's pool (sampled modes)
+  auto load_words = [&](int64_t g, uint32_t& u, uint32_t& v) {
+    if constexpr (kSamp) {
+      const uint2 w = *reinterpret_cast<const uint2*>(a.samp + 4 * g + (isp ? 0 : 2));
+      u = w.x;
+      v = w.y;
+    } else {
+      u = v = 0;
+    }
+  };
+  uint32_t cu, cv;
+  load_words(base, cu, cv);
   const int32_t last = R - 1;
   int64_t nx_arr;
   int32_t nx_p, nx_o, nx_oh;
-  uint32_t nx_c;
+  uint32_t nx_c, nx_u, nx_v;
   {
     const int64_t g = base + min(1, last);
     nx_arr = a.arrival[g];
@@ -99,6 +112,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     nx_o = a.olen[g];
     nx_oh = a.ohat[g];
     nx_c = a.cls[g];
+    load_words(g, nx_u, nx_v);
   }
   int32_t rr = 0;     // round robin: t mod (size of this lane's pool)
   double tmax = 0.0;  // latest decode end this lane recorded (time-range check)
@@ -116,6 +130,8 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     uint32_t bkey = 0xffffffffu;
     int32_t bm = 0;
     double bbusy = s[0].busy;
+    uint32_t c1 = 0, c2 = 0;  // the pool's sampled candidates
+    if constexpr (kSamp) sample_pair(cu, cv, (uint32_t)npool, c1, c2);
 #pragma unroll
     for (int m = 0; m < M; ++m) {
       const Slot& x = s[m];
@@ -124,7 +140,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
         key = policy == kPolicyLeastLoaded ? (uint32_t)x.q : ((wave + W * (lrel * M + m)) == rr ? 0u : 1u);
       } else {
         float bl;
-        if constexpr (kMode == kModeTrue)
+        if constexpr (!kTok)
           bl = (float)__builtin_fmax(x.busy - now, 0.0) * 1e-9f;
         else
           bl = tau * (float)x.pend + basec * (float)x.q;
@@ -133,6 +149,10 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
         const float size = work * (1.0f + rho * press) * sg;
         const float cost = load + size + w_q * (float)x.q;
         key = cost != cost ? 0x7fc00000u : __float_as_uint(cost);
+      }
+      if constexpr (kSamp) {
+        const uint32_t j = (uint32_t)(wave + W * (lrel * M + m));
+        key = (j == c1 || j == c2) ? key : 0xffffffffu;
       }
       key = ok[m] ? key : 0xffffffffu;
       if (m == 0) {
@@ -286,6 +306,8 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     // 7. the releases for request t+1 (slot by slot, where some lane's head
     // has finished); load request t+2
     cur = nxt;
+    cu = nx_u;
+    cv = nx_v;
 #pragma unroll
     for (int m = 0; m < M; ++m)
       if (__any(s[m].h.t <= cur.now_eff)) release_slot<kTok, kKv>(s[m], cur.now_eff, recb, tokb, base, R, dmy);
@@ -297,6 +319,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
       nx_o = a.olen[g];
       nx_oh = a.ohat[g];
       nx_c = a.cls[g];
+      load_words(g, nx_u, nx_v);
     }
   }
   const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u);

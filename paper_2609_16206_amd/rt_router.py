@@ -13,13 +13,14 @@ import ctypes as C
 import os
 from typing import Dict, Optional, Sequence
 
+import numpy as np
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("RT_ROUTER_LIB") or os.path.join(HERE, "librt_router.so")
 
 RT_OK, RT_EINVAL, RT_ENOMEM, RT_EDEVICE, RT_ERANGE, RT_EUNSUPPORTED, RT_EDATA = 0, -1, -2, -3, -4, -5, -6
-RT_POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2}
+RT_POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2, "learned_sampled": 3}
 RT_BACKLOG = {"true": 0, "proxy": 1}
 RT_POOL = {"prefill": 0, "decode": 1}
 RT_MAX_CLASSES = 8
@@ -56,7 +57,8 @@ class rt_point(C.Structure):
 class rt_trace(C.Structure):
     _fields_ = [("n_replicas", C.c_int64), ("n_requests", C.c_int64), ("offsets", C.c_void_p),
                 ("param_point", C.c_void_p), ("arrival_ns", C.c_void_p), ("prompt_len", C.c_void_p),
-                ("out_len", C.c_void_p), ("pred_out_len", C.c_void_p), ("slo_class", C.c_void_p)]
+                ("out_len", C.c_void_p), ("pred_out_len", C.c_void_p), ("slo_class", C.c_void_p),
+                ("sample_bits", C.c_void_p)]
 
 
 class rt_sim_out(C.Structure):
@@ -169,6 +171,14 @@ def _trace_struct(tr: Dict[str, torch.Tensor]) -> rt_trace:
     t.out_len = _dptr(tr["out_len"], torch.int32, "out_len")
     t.pred_out_len = _dptr(tr["pred_out_len"], torch.int32, "pred_out_len")
     t.slo_class = _dptr(tr["slo_class"], torch.uint8, "slo_class")
+    # [n_requests, 4] candidate words; torch has no general uint32 tensor, so
+    # they travel as int32 with the same bits
+    sb = tr.get("sample_bits")
+    if sb is not None and sb.dim() != 2:
+        raise ValueError("sample_bits must have shape [n_requests, 4]")
+    if sb is not None and (sb.shape[1] != 4 or sb.shape[0] != t.n_requests):
+        raise ValueError("sample_bits must have shape [n_requests, 4]")
+    t.sample_bits = _dptr(sb, torch.int32, "sample_bits")
     return t
 
 
@@ -235,8 +245,12 @@ OUT_KEYS = ("i_pre", "i_dec", "ttft_ns", "decode_span_ns")
 
 
 def to_device(trace_np: Dict, device="cuda") -> Dict[str, torch.Tensor]:
-    """Copy a numpy SoA trace to GPU tensors."""
-    return {k: torch.from_numpy(trace_np[k]).to(device) for k in TRACE_KEYS if k in trace_np}
+    """Copy a numpy SoA trace to GPU tensors (the candidate words of the
+    sampled policy, if present, as int32 with the same bits)."""
+    out = {k: torch.from_numpy(trace_np[k]).to(device) for k in TRACE_KEYS if k in trace_np}
+    if "sample_bits" in trace_np:
+        out["sample_bits"] = torch.from_numpy(trace_np["sample_bits"].view(np.int32)).to(device)
+    return out
 
 
 def alloc_outputs(n_requests: int, device="cuda") -> Dict[str, torch.Tensor]:

@@ -448,10 +448,12 @@ def tiny_sim(seed: int = 0) -> Workload:
                     [make_point(3, 3, n_classes=2)], [tiny_poisson(4.0)])
 
 
-def paper_cluster(n_replicas: int = 4096, requests: int = 10_000, seed: int = 2) -> Workload:
+def paper_cluster(n_replicas: int = 4096, requests: int = 10_000, seed: int = 2,
+                  policy: str = "learned") -> Workload:
     """2 prefill + 6 decode, mixed bursty MMPP (3 / 12 req/s, 20 s dwell)."""
-    return Workload(f"cluster-2p6d-mmpp-{n_replicas}x{requests}", seed, n_replicas, requests,
-                    [make_point(2, 6, n_classes=3)], [mixed_bursty()])
+    tag = "" if policy == "learned" else "-" + policy.replace("_", "-")
+    return Workload(f"cluster-2p6d-mmpp-{n_replicas}x{requests}{tag}", seed, n_replicas, requests,
+                    [make_point(2, 6, n_classes=3, policy=policy)], [mixed_bursty()])
 
 
 SWEEP_WIDTHS = (3, 4, 6, 8, 16, 32, 64)

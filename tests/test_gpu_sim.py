@@ -7,6 +7,7 @@ replica-range resume."""
 import numpy as np
 import pytest
 
+from paper_2609_16206_amd import rt_router as R
 from paper_2609_16206_amd import workload as W
 from tests.gpu_common import log, run_sim
 from tests.parity import check_properties, follow_replicas, goodput_recount
@@ -97,6 +98,42 @@ def test_pools_at_the_limit():
     check_properties(pts, tr, gpu)
     rep = follow_replicas(pts, tr, gpu, range(len(lengths)), gpu_goodput=g, gpu_met=met)
     log(f"pools at the limit: {rep}")
+
+
+def test_sampled_policy_mixed_with_learned():
+    """The two-candidate policy in both scoring modes, on one-wave and
+    multi-wave pool shapes, in one batch with full-argmin points (so each
+    point's kernel class is picked by its mode); follow-mode parity."""
+    shapes = [(1, 2), (2, 6), (3, 9), (5, 16), (2, 33), (33, 64), (70, 100), (128, 300)]
+    pts = []
+    for k, (P, D) in enumerate(shapes):
+        mode = ("true", "proxy")[k % 2]
+        pts.append(W.make_point(P, D, n_classes=3, policy="learned_sampled", backlog_mode=mode, kv_cap=50_000))
+        pts.append(W.make_point(P, D, n_classes=3, policy="learned", backlog_mode=mode, kv_cap=50_000))
+    lengths = [1500, 3, 700, 2000, 64, 65, 1, 999] * 4
+    tr = _ragged_trace(pts, lengths, seed=23, rate_scale=1.3)
+    W.add_sample_words(tr, 23)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    check_properties(pts, tr, gpu)
+    rep = follow_replicas(pts, tr, gpu, range(len(lengths)), gpu_goodput=g, gpu_met=met)
+    log(f"sampled policy: {rep}")
+    # every sampled placement is one of its request's two candidates
+    from oracle import oracle as O
+    off = tr["offsets"]
+    for i in range(0, len(lengths), 2):
+        P, D = pts[i % len(pts)]["n_prefill"], pts[i % len(pts)]["n_decode"]
+        for r in range(int(off[i]), min(int(off[i + 1]), int(off[i]) + 50)):
+            w = tr["sample_bits"][r]
+            assert gpu["i_pre"][r] in O.candidates(w[0], w[1], P)
+            assert gpu["i_dec"][r] in O.candidates(w[2], w[3], D)
+
+
+def test_sampled_policy_requires_words():
+    pts = [W.make_point(2, 6, policy="learned_sampled")]
+    tr = _ragged_trace(pts, [10], seed=1)
+    with pytest.raises(R.RtError):
+        run_sim(pts, tr)
 
 
 def test_overload_deep_queues():
