@@ -151,6 +151,13 @@ def simulate(pt: Dict, arrival, prompt, out, pred, cls, words=None) -> Dict[str,
         if pt["policy"] == "least_loaded":
             qs = [len(led[j]) for j in range(n_inst)]
             return int(np.argmin(qs))  # first minimum = lowest index
+        if pt["policy"] == "length_threshold":
+            part = list(range(n_inst))
+            if pool == 1 and n_inst > 1:
+                h = (n_inst + 1) // 2
+                part = part[h:] if int(pred[r]) >= int(pt["len_threshold"]) else part[:h]
+            qs = [len(led[j]) for j in part]
+            return part[int(np.argmin(qs))]
         sg = F(pt["sigma"][int(cls[r])])
         if pool == 0:
             work = F(pt["w_s"]) * F(int(prompt[r])) * F(pt["tau_pre_s"])

@@ -17,7 +17,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("RT_ORACLE_LIB") or os.path.join(HERE, "librt_oracle.so")
 MAX_CLASSES = 8
-POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2, "learned_sampled": 3}
+POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2, "learned_sampled": 3, "length_threshold": 4}
 BACKLOG = {"true": 0, "proxy": 1}
 POOL = {"prefill": 0, "decode": 1}
 
@@ -33,7 +33,8 @@ class Point(C.Structure):
                 ("policy", C.c_int32), ("backlog_mode", C.c_int32), ("router", Router),
                 ("pre_base_ns", C.c_int64), ("pre_tok_ns", C.c_int64), ("dec_tok_ns", C.c_int64),
                 ("xfer_tok_ns", C.c_int64), ("kv_cap_pre", C.c_int64), ("kv_cap_dec", C.c_int64),
-                ("slo_ttft_ns", C.c_int64 * MAX_CLASSES), ("slo_tpot_ns", C.c_int64 * MAX_CLASSES)]
+                ("slo_ttft_ns", C.c_int64 * MAX_CLASSES), ("slo_tpot_ns", C.c_int64 * MAX_CLASSES),
+                ("len_threshold", C.c_int32)]
 
 
 STAT_FIELDS = ["invalid", "near_tie_pre", "near_tie_dec", "mismatch_pre", "mismatch_dec", "first_mismatch",
@@ -94,6 +95,7 @@ def point_struct(d: Dict) -> Point:
     for i in range(MAX_CLASSES):
         p.slo_ttft_ns[i] = int(d["slo_ttft_ns"][i])
         p.slo_tpot_ns[i] = int(d["slo_tpot_ns"][i])
+    p.len_threshold = int(d.get("len_threshold", 1))
     return p
 
 

@@ -208,6 +208,20 @@ static int32_t choose(const orc_point* pt, int32_t pool, const inst_t* inst, int
       if (inst[j].queue < inst[b].queue) b = j;
     return b;
   }
+  if (pt->policy == ORC_LENGTH_THRESHOLD) {
+    /* the part of the pool this request may use: all of the prefill pool;
+     * of the decode pool, the upper half for long predicted outputs */
+    int32_t lo = 0, hi = n;
+    if (pool == ORC_DECODE && n > 1) {
+      const int32_t half = (n + 1) / 2;
+      if (ohat >= pt->len_threshold) lo = half;
+      else hi = half;
+    }
+    int32_t b = lo;
+    for (int32_t j = lo + 1; j < hi; ++j)
+      if (inst[j].queue < inst[b].queue) b = j;
+    return b;
+  }
   const orc_router* rp = &pt->router;
   const float sg = rp->sigma[c];
   const float work = pool_work(rp, pool, p, ohat);
@@ -269,6 +283,7 @@ int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
   if (pt->n_prefill < 1 || pt->n_decode < 1 || pt->n_classes < 1 ||
       pt->n_classes > ORC_MAX_CLASSES || pt->kv_cap_pre < 1 || pt->kv_cap_dec < 1)
     return -1;
+  if (pt->policy == ORC_LENGTH_THRESHOLD && pt->len_threshold < 1) return -1;
   if (n > 0 && (!arrival_ns || !prompt_len || !out_len || !pred_out_len || !slo_class || !i_pre ||
                 !i_dec || !ttft_ns || !span_ns))
     return -1;

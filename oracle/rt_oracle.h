@@ -40,7 +40,12 @@ extern "C" {
 /* ORC_LEARNED_SAMPLED: the learned score over two random candidates per pool
  * (the sampled variant Section V-E and Section VI name as the mitigation for
  * scarce pools).  The random words are inputs (see orc_candidates). */
-enum { ORC_LEARNED = 0, ORC_ROUND_ROBIN = 1, ORC_LEAST_LOADED = 2, ORC_LEARNED_SAMPLED = 3 };
+/* ORC_LENGTH_THRESHOLD: the predicted-length threshold baseline (Section
+ * IV-C), read as size-interval assignment: prefill least loaded; decode least
+ * loaded within the lower part [0, ceil(D/2)) for o^ < len_threshold, within
+ * the upper part [ceil(D/2), D) otherwise (both parts are instance 0 when
+ * D == 1). */
+enum { ORC_LEARNED = 0, ORC_ROUND_ROBIN = 1, ORC_LEAST_LOADED = 2, ORC_LEARNED_SAMPLED = 3, ORC_LENGTH_THRESHOLD = 4 };
 enum { ORC_BACKLOG_TRUE = 0, ORC_BACKLOG_PROXY = 1 };
 enum { ORC_PREFILL = 0, ORC_DECODE = 1 };
 
@@ -58,6 +63,7 @@ typedef struct {
   int64_t pre_base_ns, pre_tok_ns, dec_tok_ns, xfer_tok_ns;
   int64_t kv_cap_pre, kv_cap_dec;
   int64_t slo_ttft_ns[ORC_MAX_CLASSES], slo_tpot_ns[ORC_MAX_CLASSES];
+  int32_t len_threshold; /* ORC_LENGTH_THRESHOLD only */
 } orc_point;
 
 typedef struct {

@@ -129,6 +129,7 @@ def make_point(
     tau_dec_scale: float = 1.0,
     sigma: Optional[Sequence[float]] = None,
     link_bytes_per_s: float = LINK_BYTES_PER_S,
+    len_threshold: int = 256,
 ) -> Dict:
     """One parameter point: pool shape, router constants, physics and SLOs.
 
@@ -144,6 +145,7 @@ def make_point(
         n_decode=int(n_decode),
         n_classes=int(n_classes),
         policy=policy,
+        len_threshold=int(len_threshold),
         backlog_mode=backlog_mode,
         w_b=f32(w_b),
         w_s=f32(w_s),

@@ -167,14 +167,15 @@ def test_event_heap_bruteforce_agrees():
     for case in range(2000):
         P, D = (int(x) for x in rng.integers(1, 4, size=2))
         n = int(rng.integers(1, 17))
-        pol = ("learned", "round_robin", "least_loaded", "learned_sampled")[case % 4]
-        mode = ("true", "proxy")[(case // 4) % 2]
+        pol = ("learned", "round_robin", "least_loaded", "learned_sampled", "length_threshold")[case % 5]
+        mode = ("true", "proxy")[(case // 5) % 2]
         pt = W.make_point(P, D, n_classes=3, policy=pol, backlog_mode=mode,
                           physics=dict(pre_base_ns=int(rng.integers(0, 3)) * 10,
                                        pre_tok_ns=int(rng.integers(0, 3)) * 10,
                                        dec_tok_ns=int(rng.integers(0, 4)) * 10, kv_bytes_per_token=2048),
                           kv_cap=int(rng.integers(1, 50)), w_q=float(rng.choice([0.0, 1e-3, 1.0])),
-                          rho=float(rng.choice([0.0, 1.0, 3.0])), w_b=float(rng.choice([0.0, 1.0, 1e7])))
+                          rho=float(rng.choice([0.0, 1.0, 3.0])), w_b=float(rng.choice([0.0, 1.0, 1e7])),
+                          len_threshold=int(rng.integers(1, 6)))
         pt["xfer_tok_ns"] = int(rng.integers(0, 3)) * 10
         arr = np.sort(rng.integers(0, 8, n) * 10).astype(np.int64)
         p = rng.integers(1, 5, n).astype(np.int32)
