@@ -66,10 +66,15 @@ typedef enum {
   RT_POLICY_LEARNED = 0,      /* the marginal-cost scorer (Section III-A)              */
   RT_POLICY_ROUND_ROBIN = 1,  /* request r goes to instance r mod N (Section IV-C)     */
   RT_POLICY_LEAST_LOADED = 2, /* fewest in-flight requests, lowest index on ties       */
-  RT_POLICY_LEARNED_SAMPLED = 3 /* the scorer over two random candidates per pool: the
+  RT_POLICY_LEARNED_SAMPLED = 3, /* the scorer over two random candidates per pool: the
                                    sampled variant that Section V-E and Section VI give
                                    as the mitigation for scarce pools (candidates: see
                                    rt_sim_run_replicas)                                */
+  RT_POLICY_LENGTH_THRESHOLD = 4 /* the predicted-length threshold baseline of Section
+                                   IV-C, read as size-interval assignment: requests
+                                   with o^_r >= len_threshold use the upper part of the
+                                   decode pool, the others the lower part (see
+                                   rt_sim_run_replicas); least loaded within a part   */
 } rt_policy;
 
 typedef enum {
@@ -111,6 +116,10 @@ typedef struct {
   int32_t backlog_mode;        /* rt_backlog_mode                         */
   rt_router_params router;
   rt_physics phys;
+  int32_t len_threshold;       /* RT_POLICY_LENGTH_THRESHOLD: predicted output
+                                  tokens at which a request counts as long
+                                  (>= 1); unread by the other policies      */
+  int32_t reserved;            /* set to 0                                */
 } rt_point;
 
 typedef struct rt_sim rt_sim; /* opaque: device copies of the points, scratch, flag word */
@@ -174,6 +183,12 @@ typedef struct {
  * (two distinct instances, every ordered pair equally likely up to a bias of
  * n / 2^32), and the request goes to the cheaper of the two, the lower index
  * on equal cost.  With n <= 2 this is the full argmin.
+ * Under RT_POLICY_LENGTH_THRESHOLD the prefill pool is least loaded (fewest
+ * requests in flight, lowest index); the decode pool of D instances is cut
+ * into a lower part [0, ceil(D/2)) and an upper part [ceil(D/2), D) (with
+ * D == 1 both parts are instance 0), a request with o^_r >= len_threshold
+ * goes to the least loaded instance of the upper part, any other request to
+ * the least loaded of the lower part.
  * The call reads offsets and param_point back to the host to plan the launch
  * (it synchronizes `hip_stream` for that), validates them (RT_EINVAL), then
  * enqueues the simulation on `hip_stream` and returns.  Scratch memory grows

@@ -49,7 +49,8 @@ std::string check_point(const rt_point& p) {
   if (p.n_prefill < 1 || p.n_decode < 1) return "pool sizes must be >= 1";
   if (p.n_prefill > RT_MAX_POOL || p.n_decode > RT_MAX_POOL) return "pool wider than RT_MAX_POOL";
   if (p.n_classes < 1 || p.n_classes > RT_MAX_CLASSES) return "n_classes must be in [1, RT_MAX_CLASSES]";
-  if (p.policy < RT_POLICY_LEARNED || p.policy > RT_POLICY_LEARNED_SAMPLED) return "unknown policy";
+  if (p.policy < RT_POLICY_LEARNED || p.policy > RT_POLICY_LENGTH_THRESHOLD) return "unknown policy";
+  if (p.policy == RT_POLICY_LENGTH_THRESHOLD && p.len_threshold < 1) return "len_threshold must be >= 1";
   if (p.backlog_mode != RT_BACKLOG_TRUE && p.backlog_mode != RT_BACKLOG_PROXY) return "unknown backlog_mode";
   const rt_router_params& r = p.router;
   const float f[] = {r.w_b, r.w_s, r.w_q, r.rho, r.tau_pre_s, r.tau_dec_s, r.pre_base_s};
@@ -75,6 +76,7 @@ rt::DevPoint to_dev(const rt_point& p) {
   d.D = p.n_decode;
   d.n_classes = p.n_classes;
   d.policy = p.policy;
+  d.len_thr = p.len_threshold;
   d.mode = p.backlog_mode;
   // Adding +0.0f turns a -0.0f weight into +0.0f (and changes nothing else):
   // with every factor then +0 or positive, no cost is -0 and the kernels can

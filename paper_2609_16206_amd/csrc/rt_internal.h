@@ -12,7 +12,7 @@ constexpr int kMaxClasses = 8;
 // One parameter point as the kernels read it: the public rt_point plus
 // host-computed constants (reciprocal cache capacities).
 struct DevPoint {
-  int32_t P, D, n_classes, policy, mode, pad0[3];
+  int32_t P, D, n_classes, policy, mode, len_thr, pad0[2];
   float w_b, w_s, w_q, rho;
   float tau_pre, tau_dec, pre_base;
   float inv_cap_pre, inv_cap_dec;  // 1.0f / (float)capacity, rounded once
@@ -25,7 +25,13 @@ struct DevPoint {
 enum : uint32_t { kFlagRejected = 1u, kFlagBadTrace = 2u, kFlagTimeRange = 4u };
 
 // rt_policy values as the kernels read them from DevPoint::policy.
-enum : int32_t { kPolicyLearned = 0, kPolicyRoundRobin = 1, kPolicyLeastLoaded = 2, kPolicyLearnedSampled = 3 };
+enum : int32_t {
+  kPolicyLearned = 0,
+  kPolicyRoundRobin = 1,
+  kPolicyLeastLoaded = 2,
+  kPolicyLearnedSampled = 3,
+  kPolicyLengthThreshold = 4
+};
 
 // Arguments of the replica-simulation kernels.
 struct SimArgs {

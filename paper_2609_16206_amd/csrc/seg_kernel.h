@@ -268,6 +268,9 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   const int pid = (live && a.param_point) ? a.param_point[rep] : 0;
   const DevPoint& pt = a.points[pid];
   const int32_t P = pt.P, D = pt.D, ncls = pt.n_classes, policy = pt.policy;
+  const bool thr = policy == kPolicyLengthThreshold;
+  const int32_t half_d = (D + 1) / 2;  // first instance of the decode pool's upper part
+  const int32_t len_thr = pt.len_thr;
   const int32_t LP = (P + M - 1) / M;  // lanes holding prefill instances
   const bool isp = sl < LP;
   const int32_t j0 = (isp ? sl : sl - LP) * M;  // this lane's first instance in its pool
@@ -356,6 +359,7 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     const int32_t cnt = isp ? p : oh;           // priced tokens of the pool
     const float work = w_s * (float)cnt * tau;  // w_s * p * tau_pre, or w_s * o^ * tau_dec
     const double need = (double)(isp ? p : poh);
+    const bool long_req = oh >= len_thr;  // length threshold: the upper part
     uint32_t bkey = 0xffffffffu;
     int32_t bm = 0;
     double bbusy = s[0].busy;
@@ -366,7 +370,12 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
       const Slot& x = s[m];
       uint32_t key;
       if constexpr (kMode == kModeBase) {
-        key = policy == kPolicyLeastLoaded ? (uint32_t)x.q : ((j0 + m) == rr ? 0u : 1u);
+        // round robin; least loaded; or least loaded within the decode
+        // part the request's predicted length picks (length threshold)
+        const int32_t j = (j0 + m);
+        key = policy == kPolicyRoundRobin ? (j == rr ? 0u : 1u) : (uint32_t)x.q;
+        const bool part = D == 1 || ((j >= half_d) == long_req);
+        key = (thr && !isp && !part) ? 0xffffffffu : key;
       } else {
         float bl;
         if constexpr (!kTok)

@@ -20,7 +20,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("RT_ROUTER_LIB") or os.path.join(HERE, "librt_router.so")
 
 RT_OK, RT_EINVAL, RT_ENOMEM, RT_EDEVICE, RT_ERANGE, RT_EUNSUPPORTED, RT_EDATA = 0, -1, -2, -3, -4, -5, -6
-RT_POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2, "learned_sampled": 3}
+RT_POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2, "learned_sampled": 3, "length_threshold": 4}
 RT_BACKLOG = {"true": 0, "proxy": 1}
 RT_POOL = {"prefill": 0, "decode": 1}
 RT_MAX_CLASSES = 8
@@ -51,7 +51,7 @@ class rt_physics(C.Structure):
 class rt_point(C.Structure):
     _fields_ = [("n_prefill", C.c_int32), ("n_decode", C.c_int32), ("n_classes", C.c_int32),
                 ("policy", C.c_int32), ("backlog_mode", C.c_int32), ("router", rt_router_params),
-                ("phys", rt_physics)]
+                ("phys", rt_physics), ("len_threshold", C.c_int32), ("reserved", C.c_int32)]
 
 
 class rt_trace(C.Structure):
@@ -146,6 +146,8 @@ def point(d: Dict) -> rt_point:
     for i in range(RT_MAX_CLASSES):
         p.phys.slo_ttft_ns[i] = int(d["slo_ttft_ns"][i])
         p.phys.slo_tpot_ns[i] = int(d["slo_tpot_ns"][i])
+    p.len_threshold = int(d.get("len_threshold", 1))
+    p.reserved = 0
     return p
 
 

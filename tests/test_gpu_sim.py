@@ -129,6 +129,31 @@ def test_sampled_policy_mixed_with_learned():
             assert gpu["i_dec"][r] in O.candidates(w[2], w[3], D)
 
 
+def test_length_threshold_policy():
+    """The length-threshold baseline on one-wave and multi-wave shapes, with
+    thresholds that split the mixed traffic; follow-mode parity (exact:
+    the policy has no floating point) and the part each request used."""
+    shapes = [(1, 1), (2, 2), (2, 6), (3, 9), (5, 16), (33, 64), (70, 100), (128, 300)]
+    pts = [W.make_point(P, D, n_classes=3, policy="length_threshold", len_threshold=(64, 256, 1000)[k % 3])
+           for k, (P, D) in enumerate(shapes)]
+    lengths = [1500, 3, 700, 2000, 64, 65, 1, 999] * 2
+    tr = _ragged_trace(pts, lengths, seed=31, rate_scale=1.2)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    check_properties(pts, tr, gpu)
+    rep = follow_replicas(pts, tr, gpu, range(len(lengths)), gpu_goodput=g, gpu_met=met)
+    log(f"length threshold: {rep}")
+    assert rep["near_ties"] == 0
+    off = tr["offsets"]
+    for i in range(len(lengths)):
+        pt = pts[i % len(pts)]
+        D, thr = pt["n_decode"], pt["len_threshold"]
+        sl = slice(int(off[i]), int(off[i + 1]))
+        if D > 1:
+            lng = tr["pred_out_len"][sl] >= thr
+            assert np.all((gpu["i_dec"][sl] >= (D + 1) // 2) == lng)
+
+
 def test_sampled_policy_requires_words():
     pts = [W.make_point(2, 6, policy="learned_sampled")]
     tr = _ragged_trace(pts, [10], seed=1)
