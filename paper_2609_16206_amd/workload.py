@@ -271,6 +271,31 @@ def mixed_bursty(calm: float = 3.0, burst: float = 12.0) -> Traffic:
     )
 
 
+# The other workload families of Table I as Poisson streams (the lengths are
+# our proposal; the paper characterizes them only qualitatively).
+DOC_PROMPT = LogNormal(7.6, 0.5, 256, 4096)  # long documents, up to 4k in
+DOC_OUTPUT = LogNormal(4.5, 0.8, 1, 4096)    # short answers
+
+
+def chat(rate: float) -> Traffic:
+    return Traffic((CHAT_PROMPT,), (CHAT_OUTPUT,), (1.0,), (0.5, 0.3, 0.2), "poisson", (rate,))
+
+
+def document(rate: float) -> Traffic:
+    return Traffic((DOC_PROMPT,), (DOC_OUTPUT,), (1.0,), (0.5, 0.3, 0.2), "poisson", (rate,))
+
+
+def reasoning(rate: float) -> Traffic:
+    return Traffic((REASON_PROMPT,), (REASON_OUTPUT,), (1.0,), (0.5, 0.3, 0.2), "poisson", (rate,))
+
+
+def with_predictor_sigma(traffic: Traffic, sigma: float) -> Traffic:
+    """The same traffic with the output-length predictor's log-normal error
+    sigma (o^ = o * exp(sigma * z))."""
+    return Traffic(traffic.prompt, traffic.output, traffic.mix, traffic.class_probs, traffic.arrival,
+                   traffic.rates, traffic.dwell_mean_s, float(sigma))
+
+
 def tiny_poisson(rate: float = 4.0) -> Traffic:
     return Traffic(
         prompt=(LogNormal(6.0, 1.0, 16, 8192),),

@@ -1,0 +1,56 @@
+"""Host-side parts of the experiment drivers (CPU): the calibration fit
+(Section III-B) and the batch layout of a grid."""
+import numpy as np
+
+from paper_2609_16206_amd import experiments as E
+from paper_2609_16206_amd import workload as W
+
+
+def test_fit_recovers_noiseless_constants():
+    pt = W.make_point(2, 4)
+    fit = E.fit_service_constants(**E.latency_curves(pt, n=300))
+    assert abs(fit["pre_base_ns"] - pt["pre_base_ns"]) < 1e-3 * pt["pre_base_ns"]
+    assert abs(fit["pre_tok_ns"] - pt["pre_tok_ns"]) < 1e-6 * pt["pre_tok_ns"]
+    assert abs(fit["dec_tok_ns"] - pt["dec_tok_ns"]) < 1e-9 * pt["dec_tok_ns"]
+    # the calibrated router prices are the physics' own (Section III-B)
+    q = E.calibrated_point(pt, fit)
+    assert q["tau_dec_s"] == pt["tau_dec_s"] and q["tau_pre_s"] == pt["tau_pre_s"]
+
+
+def test_fit_under_noise_is_close():
+    pt = W.make_point(2, 4)
+    fit = E.fit_service_constants(**E.latency_curves(pt, n=4000, noise=0.05, seed=3))
+    assert abs(fit["dec_tok_ns"] / pt["dec_tok_ns"] - 1) < 0.01
+    assert abs(fit["pre_tok_ns"] / pt["pre_tok_ns"] - 1) < 0.05
+
+
+def test_mispriced_fit_is_detectable():
+    """A point whose physics differs from the router's prices (the paper's
+    7.4x decode mismatch) is repaired by fitting to the physics."""
+    pt = W.make_point(2, 4, tau_dec_scale=1 / 7.4)
+    assert pt["tau_dec_s"] < pt["dec_tok_ns"] * 1e-9 / 7
+    q = E.calibrated_point(pt, E.fit_service_constants(**E.latency_curves(pt)))
+    assert abs(q["tau_dec_s"] / (pt["dec_tok_ns"] * 1e-9) - 1) < 1e-6
+
+
+def test_grid_trace_layout_and_streams():
+    cells = E.policy_cells(2, 3, W.mixed_bursty())
+    tr = E.build_trace(cells, replicas=3, requests=50, seed=5)
+    assert tr["offsets"][-1] == len(cells) * 3 * 50
+    assert list(tr["param_point"]) == [c for c in range(len(cells)) for _ in range(3)]
+    assert tr["sample_bits"].shape == (len(cells) * 3 * 50, 4)
+    # cells draw disjoint streams, the same cell draws the same ones
+    a = tr["arrival_ns"][:50]
+    assert not np.array_equal(a, tr["arrival_ns"][150:200])
+    tr2 = E.build_trace(cells, replicas=3, requests=50, seed=5)
+    assert np.array_equal(tr["prompt_len"], tr2["prompt_len"])
+
+
+def test_noise_cells_change_only_the_prediction():
+    cells = E.noise_cells(2, 3, W.mixed_bursty(), sigmas=(0.0, 1.5))
+    t0 = E.build_trace(cells[:1], 1, 200, seed=2)
+    t1 = E.build_trace(cells[1:], 1, 200, seed=2)
+    for k in ("arrival_ns", "prompt_len", "out_len", "slo_class"):
+        assert np.array_equal(t0[k], t1[k]), k
+    assert np.array_equal(t0["pred_out_len"], np.maximum(1, t0["out_len"]))
+    assert not np.array_equal(t1["pred_out_len"], t0["pred_out_len"])

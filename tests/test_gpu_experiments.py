@@ -1,0 +1,44 @@
+"""Experiment drivers on the GPU: a batched policy grid agrees with the
+oracle replica by replica, and the saturation search finds the scale where
+round robin is mid-collapse."""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2609_16206_amd import experiments as E
+from paper_2609_16206_amd import workload as W
+from tests.gpu_common import log
+
+pytestmark = pytest.mark.gpu
+
+
+def test_policy_grid_matches_oracle():
+    traf = W.mixed_bursty().scaled(1.3)
+    cells = E.policy_cells(2, 4, traf) + E.ablation_cells(2, 4, traf)[1:] + E.noise_cells(2, 4, traf, (0.0, 1.5))
+    rows, tr, out, g = E.run_cells(cells, replicas=3, requests=1500, seed=4, return_trace=True)
+    log("grid: " + ", ".join(f"{r['label']} {r['mean']:.3f}" for r in rows))
+    ref = O.sim_trace([c.point for c in cells], tr, threads=16)
+    for i, (o, st, gg, met) in ref.items():
+        sl = slice(int(tr["offsets"][i]), int(tr["offsets"][i + 1]))
+        assert np.array_equal(o["i_pre"], out["i_pre"][sl]) and np.array_equal(o["i_dec"], out["i_dec"][sl]), i
+        assert np.array_equal(o["ttft_ns"], out["ttft_ns"][sl]) and np.array_equal(o["decode_span_ns"],
+                                                                                   out["decode_span_ns"][sl]), i
+        assert gg == g[i], i
+
+
+def test_saturation_search_brackets_round_robin_collapse():
+    pt = W.make_point(2, 4, n_classes=3)
+    traf = W.mixed_bursty()
+    res = E.saturation_scale(pt, traf, target=0.5, replicas=16, requests=3000, seed=1)
+    log(f"saturation: scale {res['scale']}, probes {[(round(s, 3), round(g, 3)) for s, g in res['probes']]}")
+    assert res["scale"] is not None
+    s0, s1 = res["bracket"]
+    assert s0 < res["scale"] <= s1
+    # goodput falls with load across the probed grid (allowing replica noise)
+    g = np.array([x for _, x in res["probes"]])
+    assert g[0] > 0.5 > g[-1]
+    assert np.all(np.diff(g) < 0.05)
+    # at the found scale round robin is near the target
+    rows = E.run_cells([E.Cell("rr", dict(pt, policy="round_robin"), traf.scaled(res["scale"]))],
+                       replicas=16, requests=3000, seed=1)
+    assert abs(rows[0]["mean"] - 0.5) < 0.1, rows
