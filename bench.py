@@ -161,7 +161,7 @@ def bench_sim(args):
         roof = dict(bound="alu", achieved=alg_ops / kernel_s / 1e12, peak=ALU_PEAK / 1e12, unit="Tlane-op/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = _traffic("sim", args.workload, SIM_SOURCES)
-    roof["kernel"] = "rt::sim_kernel (all classes of one rt_sim_run_replicas call)"
+    roof["kernel"] = "rt::seg::seg_kernel / wseg_kernel (every class one rt_sim_run_replicas call launches)"
     roof["kernel_ms"] = kernel_s * 1e3
     roof["alg_bytes"] = alg_bytes
     roof["alg_lane_ops"] = alg_ops
