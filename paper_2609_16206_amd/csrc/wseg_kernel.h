@@ -217,10 +217,16 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     const int32_t mp = qp - (qp / M) * M, md = qd - (qd / M) * M;  // slots
 
     // 4. the successors loaded during request t's releases (slots where any
-    // lane loaded some)
+    // lane loaded some; every slot's test is made before the first branch,
+    // so that the scalar branches wait for one vector compare, not one each)
+    {
+      uint64_t any_lq[M];
 #pragma unroll
-    for (int m = 0; m < M; ++m)
-      if (__any(s[m].lq >= 2)) merge_pending(s[m]);
+      for (int m = 0; m < M; ++m) any_lq[m] = __ballot(s[m].lq >= 2);
+#pragma unroll
+      for (int m = 0; m < M; ++m)
+        if (any_lq[m]) merge_pending(s[m]);
+    }
 
     // 5. request t+1: check and sigma (its features are waited for here,
     // ahead of the stores below, which the compiler's waits do not count)
@@ -317,9 +323,15 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     cur = nxt;
     cu = nx_u;
     cv = nx_v;
+    {
+      // (slots release independently, so all tests come first)
+      uint64_t any_done[M];
 #pragma unroll
-    for (int m = 0; m < M; ++m)
-      if (__any(s[m].h.t <= cur.now_eff)) release_slot<kTok, kKv>(s[m], cur.now_eff, recb, tokb, base, R, dmy);
+      for (int m = 0; m < M; ++m) any_done[m] = __ballot(s[m].h.t <= cur.now_eff);
+#pragma unroll
+      for (int m = 0; m < M; ++m)
+        if (any_done[m]) release_slot<kTok, kKv>(s[m], cur.now_eff, recb, tokb, base, R, dmy);
+    }
     release_more<M, kTok, kKv>(__any(head_min(s) <= cur.now_eff), s, cur.now_eff, recb, tokb, base, R, dmy);
     {
       const int64_t g = base + min(t + 2, last);
