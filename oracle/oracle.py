@@ -20,6 +20,7 @@ MAX_CLASSES = 8
 POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2, "learned_sampled": 3, "length_threshold": 4}
 BACKLOG = {"true": 0, "proxy": 1}
 POOL = {"prefill": 0, "decode": 1}
+SERVICE = {"serial": 0, "batched": 1}
 
 
 class Router(C.Structure):
@@ -34,7 +35,8 @@ class Point(C.Structure):
                 ("pre_base_ns", C.c_int64), ("pre_tok_ns", C.c_int64), ("dec_tok_ns", C.c_int64),
                 ("xfer_tok_ns", C.c_int64), ("kv_cap_pre", C.c_int64), ("kv_cap_dec", C.c_int64),
                 ("slo_ttft_ns", C.c_int64 * MAX_CLASSES), ("slo_tpot_ns", C.c_int64 * MAX_CLASSES),
-                ("len_threshold", C.c_int32)]
+                ("len_threshold", C.c_int32), ("service", C.c_int32), ("beta_pre", C.c_double),
+                ("beta_dec", C.c_double)]
 
 
 STAT_FIELDS = ["invalid", "near_tie_pre", "near_tie_dec", "mismatch_pre", "mismatch_dec", "first_mismatch",
@@ -64,6 +66,8 @@ def lib():
         L.orc_sim_replica.argtypes = [C.POINTER(Point), C.c_int64, P, P, P, P, P, P, P, P, C.c_double,
                                       P, P, P, P, C.POINTER(Stats)]
         L.orc_sim_replica.restype = C.c_int
+        L.orc_sim_replica_batched.argtypes = L.orc_sim_replica.argtypes
+        L.orc_sim_replica_batched.restype = C.c_int
         L.orc_goodput.argtypes = [C.POINTER(Point), C.c_int64, P, P, P, P, C.POINTER(C.c_double)]
         L.orc_goodput.restype = C.c_int64
         _lib = L
@@ -96,6 +100,10 @@ def point_struct(d: Dict) -> Point:
         p.slo_ttft_ns[i] = int(d["slo_ttft_ns"][i])
         p.slo_tpot_ns[i] = int(d["slo_tpot_ns"][i])
     p.len_threshold = int(d.get("len_threshold", 1))
+    sv = d.get("service", "serial")
+    p.service = SERVICE[sv] if isinstance(sv, str) else int(sv)
+    p.beta_pre = float(d.get("beta_pre", 0.0))
+    p.beta_dec = float(d.get("beta_dec", 0.0))
     return p
 
 
@@ -133,7 +141,9 @@ def score(router: Dict, pool: str, backlog_s, queue, kv_occ, kv_cap: int, n_inst
 def sim_replica(point: Dict, arrival_ns, prompt_len, out_len, pred_out_len, slo_class,
                 follow_pre=None, follow_dec=None, tie_rel: float = 1e-6, sample_bits=None):
     """One replica; returns (dict of outputs, dict of stats).  ``sample_bits``
-    ([n, 4] uint32) is required for the sampled policy."""
+    ([n, 4] uint32) is required for the sampled policy.  The point's
+    ``service`` ("serial", the default, or "batched") picks the service
+    model."""
     a = np.ascontiguousarray(arrival_ns, np.int64)
     n = a.size
     arrs = [np.ascontiguousarray(x, t) for x, t in ((prompt_len, np.int32), (out_len, np.int32),
@@ -145,11 +155,12 @@ def sim_replica(point: Dict, arrival_ns, prompt_len, out_len, pred_out_len, slo_
     sb = None if sample_bits is None else np.ascontiguousarray(sample_bits, np.uint32).reshape(n, 4)
     st = Stats()
     pst = point_struct(point)
-    rc = lib().orc_sim_replica(C.byref(pst), n, _ptr(a), *[_ptr(x) for x in arrs], _ptr(sb), _ptr(fp), _ptr(fd),
-                               float(tie_rel), _ptr(out["i_pre"]), _ptr(out["i_dec"]), _ptr(out["ttft_ns"]),
-                               _ptr(out["decode_span_ns"]), C.byref(st))
+    fn = lib().orc_sim_replica_batched if pst.service == SERVICE["batched"] else lib().orc_sim_replica
+    rc = fn(C.byref(pst), n, _ptr(a), *[_ptr(x) for x in arrs], _ptr(sb), _ptr(fp), _ptr(fd),
+            float(tie_rel), _ptr(out["i_pre"]), _ptr(out["i_dec"]), _ptr(out["ttft_ns"]),
+            _ptr(out["decode_span_ns"]), C.byref(st))
     if rc != 0:
-        raise ValueError(f"orc_sim_replica failed (rc={rc})")
+        raise ValueError(f"{fn.__name__} failed (rc={rc})")
     return out, {f: int(getattr(st, f)) for f in STAT_FIELDS}
 
 

@@ -180,46 +180,49 @@ static void free_pool(inst_t* a, int32_t n) {
 /* backlog(d): seconds of work already committed to d.  True mode reads the
  * simulation clock (busy-until minus now); proxy mode prices the in-flight
  * ledger with the router's own constants (Section VI). */
-static float backlog_of(const orc_point* pt, int32_t pool, const inst_t* s, int64_t now) {
+/* The proxy's ledger backlog of an instance with `queue` requests and `pend`
+ * priced tokens in flight (the same in both service models). */
+static float ledger_backlog(const orc_point* pt, int32_t pool, int64_t queue, int64_t pend) {
   const orc_router* rp = &pt->router;
+  if (pool == ORC_PREFILL) return rp->tau_pre_s * (float)pend + rp->pre_base_s * (float)queue;
+  return rp->tau_dec_s * (float)pend;
+}
+
+static float backlog_of(const orc_point* pt, int32_t pool, const inst_t* s, int64_t now) {
   if (pt->backlog_mode == ORC_BACKLOG_TRUE) {
     int64_t d = s->busy - now;
     if (d < 0) d = 0;
     return (float)d * 1e-9f;
   }
-  if (pool == ORC_PREFILL) return rp->tau_pre_s * (float)s->pend + rp->pre_base_s * (float)s->queue;
-  return rp->tau_dec_s * (float)s->pend;
+  return ledger_backlog(pt, pool, s->queue, s->pend);
 }
 
-/* Own choice for one pool.  Returns the argmin over the offered instances
- * (every instance, or under the sampled policy the two candidates drawn from
- * `words`, returned in cand[]); fills cost[] (learned policies only) and
- * reports whether the best two offered costs are within tie_rel. */
-static int32_t choose(const orc_point* pt, int32_t pool, const inst_t* inst, int32_t n, int64_t r,
-                      int64_t now, int32_t p, int32_t ohat, uint8_t c, const uint32_t* words, double tie_rel,
-                      float* cost, int32_t* cand, int* tie, int* close) {
+/* Own choice for one pool from its instances' features (backlog in
+ * seconds, requests in flight, cache tokens held).  Returns the argmin over
+ * the offered instances (every instance, or under the sampled policy the two
+ * candidates drawn from `words`, returned in cand[]); fills cost[] (learned
+ * policies only) and reports whether the best two offered costs are equal or
+ * within tie_rel. */
+static int32_t choose(const orc_point* pt, int32_t pool, int32_t n, int64_t r, const float* backlog,
+                      const int64_t* queue, const int64_t* kv, int32_t p, int32_t ohat, uint8_t c,
+                      const uint32_t* words, double tie_rel, float* cost, int32_t* cand, int* tie, int* close) {
   *tie = 0;
   *close = 0;
   cand[0] = cand[1] = -1;
   if (pt->policy == ORC_ROUND_ROBIN) return (int32_t)(r % n);
-  if (pt->policy == ORC_LEAST_LOADED) {
-    int32_t b = 0;
-    for (int32_t j = 1; j < n; ++j)
-      if (inst[j].queue < inst[b].queue) b = j;
-    return b;
-  }
-  if (pt->policy == ORC_LENGTH_THRESHOLD) {
-    /* the part of the pool this request may use: all of the prefill pool;
-     * of the decode pool, the upper half for long predicted outputs */
+  if (pt->policy == ORC_LEAST_LOADED || pt->policy == ORC_LENGTH_THRESHOLD) {
+    /* the part of the pool this request may use: everything, except under
+     * the threshold policy on the decode pool, where long predicted outputs
+     * take the upper half and the others the lower half */
     int32_t lo = 0, hi = n;
-    if (pool == ORC_DECODE && n > 1) {
+    if (pt->policy == ORC_LENGTH_THRESHOLD && pool == ORC_DECODE && n > 1) {
       const int32_t half = (n + 1) / 2;
       if (ohat >= pt->len_threshold) lo = half;
       else hi = half;
     }
     int32_t b = lo;
     for (int32_t j = lo + 1; j < hi; ++j)
-      if (inst[j].queue < inst[b].queue) b = j;
+      if (queue[j] < queue[b]) b = j;
     return b;
   }
   const orc_router* rp = &pt->router;
@@ -232,8 +235,7 @@ static int32_t choose(const orc_point* pt, int32_t pool, const inst_t* inst, int
   if (sampled) orc_candidates(words[0], words[1], n, &cand[0], &cand[1]);
   int32_t b = -1, b2 = -1;
   for (int32_t j = 0; j < n; ++j) {
-    cost[j] = cost_eq(rp, backlog_of(pt, pool, &inst[j], now), work, sg, inst[j].kv, k, inv_cap,
-                      inst[j].queue);
+    cost[j] = cost_eq(rp, backlog[j], work, sg, kv[j], k, inv_cap, queue[j]);
     if (sampled && j != cand[0] && j != cand[1]) continue; /* not offered */
     if (b < 0) {
       b = j;
@@ -251,6 +253,16 @@ static int32_t choose(const orc_point* pt, int32_t pool, const inst_t* inst, int
       *close = 1;
   }
   return b;
+}
+
+/* The serial model's features of one pool at time `now`. */
+static void serial_features(const orc_point* pt, int32_t pool, const inst_t* inst, int32_t n, int64_t now,
+                            float* backlog, int64_t* queue, int64_t* kv) {
+  for (int32_t j = 0; j < n; ++j) {
+    backlog[j] = backlog_of(pt, pool, &inst[j], now);
+    queue[j] = inst[j].queue;
+    kv[j] = inst[j].kv;
+  }
 }
 
 /* Adopt an external placement g in place of the own choice m. */
@@ -295,8 +307,12 @@ int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
   inst_t* dec = (inst_t*)calloc((size_t)D, sizeof(inst_t));
   float* cost_pre = (float*)calloc((size_t)P, sizeof(float));
   float* cost_dec = (float*)calloc((size_t)D, sizeof(float));
+  const int32_t N = P > D ? P : D;
+  float* f_backlog = (float*)calloc((size_t)N, sizeof(float));
+  int64_t* f_queue = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+  int64_t* f_kv = (int64_t*)calloc((size_t)N, sizeof(int64_t));
   int rc = 0;
-  if (!pre || !dec || !cost_pre || !cost_dec) {
+  if (!pre || !dec || !cost_pre || !cost_dec || !f_backlog || !f_queue || !f_kv) {
     rc = -2;
     goto done;
   }
@@ -326,11 +342,14 @@ int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
     int tie, close;
     int32_t cand_pre[2], cand_dec[2];
     const uint32_t* w = sample_bits ? sample_bits + 4 * r : NULL;
-    int32_t ip = choose(pt, ORC_PREFILL, pre, P, r, now, p, oh, c, w, tie_rel, cost_pre, cand_pre, &tie, &close);
+    serial_features(pt, ORC_PREFILL, pre, P, now, f_backlog, f_queue, f_kv);
+    int32_t ip = choose(pt, ORC_PREFILL, P, r, f_backlog, f_queue, f_kv, p, oh, c, w, tie_rel, cost_pre, cand_pre,
+                        &tie, &close);
     st->tie_pre += tie;
     st->close_pre += close;
-    int32_t id = choose(pt, ORC_DECODE, dec, D, r, now, p, oh, c, w ? w + 2 : NULL, tie_rel, cost_dec, cand_dec,
-                        &tie, &close);
+    serial_features(pt, ORC_DECODE, dec, D, now, f_backlog, f_queue, f_kv);
+    int32_t id = choose(pt, ORC_DECODE, D, r, f_backlog, f_queue, f_kv, p, oh, c, w ? w + 2 : NULL, tie_rel,
+                        cost_dec, cand_dec, &tie, &close);
     st->tie_dec += tie;
     st->close_dec += close;
     if (follow_pre)
@@ -392,6 +411,9 @@ done:
   free_pool(dec, D);
   free(cost_pre);
   free(cost_dec);
+  free(f_backlog);
+  free(f_queue);
+  free(f_kv);
   return rc;
 }
 
@@ -413,4 +435,350 @@ int64_t orc_goodput(const orc_point* pt, int64_t n, const int32_t* out_len,
   }
   if (goodput) *goodput = n > 0 ? (double)met / (double)n : 0.0;
   return met;
+}
+
+
+/* ------------------------------------------------------------------------ */
+/* Continuous batching in both stages (Section VI): processor sharing with a */
+/* batch-dependent speed.  See rt_oracle.h for the model.                   */
+/* ------------------------------------------------------------------------ */
+
+/* A batch member: the virtual time at which it finishes (virtual time
+ * counts the stand-alone service each member of the batch has received). */
+typedef struct {
+  double f;
+  int64_t r;
+} bmember;
+
+/* A KV transfer on its way to a decode instance: the time it lands. */
+typedef struct {
+  double t;
+  int64_t r;
+} bjoin;
+
+typedef struct {
+  double v, t_last;  /* virtual time, valid at time t_last                  */
+  bmember* act;      /* the batch, sorted by (f, r)                          */
+  int64_t nact, cap;
+  bjoin* wait;       /* decode only: transfers in flight, sorted by (t, r)   */
+  int64_t nwait, wcap;
+  int64_t owed_wait; /* decode only: stand-alone work (ns) of the requests
+                        routed here that have not joined the batch yet      */
+  int64_t queue, kv, pend;
+} binst;
+
+/* Per-request time factor of a batch of b: 1 + beta (b - 1). */
+static double slowdown(double beta, int64_t b) { return 1.0 + beta * (double)(b - 1); }
+
+static int grow(void** a, int64_t* cap, size_t sz) {
+  int64_t nc = *cap ? 2 * *cap : 16;
+  void* p = realloc(*a, (size_t)nc * sz);
+  if (!p) return -1;
+  *a = p;
+  *cap = nc;
+  return 0;
+}
+
+static int batch_insert(binst* s, double f, int64_t r) {
+  if (s->nact == s->cap && grow((void**)&s->act, &s->cap, sizeof(bmember))) return -1;
+  int64_t i = s->nact;
+  while (i > 0 && (s->act[i - 1].f > f || (s->act[i - 1].f == f && s->act[i - 1].r > r))) {
+    s->act[i] = s->act[i - 1];
+    i--;
+  }
+  s->act[i].f = f;
+  s->act[i].r = r;
+  s->nact++;
+  return 0;
+}
+
+static int wait_insert(binst* s, double t, int64_t r) {
+  if (s->nwait == s->wcap && grow((void**)&s->wait, &s->wcap, sizeof(bjoin))) return -1;
+  int64_t i = s->nwait;
+  while (i > 0 && (s->wait[i - 1].t > t || (s->wait[i - 1].t == t && s->wait[i - 1].r > r))) {
+    s->wait[i] = s->wait[i - 1];
+    i--;
+  }
+  s->wait[i].t = t;
+  s->wait[i].r = r;
+  s->nwait++;
+  return 0;
+}
+
+/* Bring the instance's virtual time to time t, with no event in between. */
+static void b_advance(binst* s, double beta, double t) {
+  if (s->nact > 0) s->v += (t - s->t_last) / slowdown(beta, s->nact);
+  s->t_last = t;
+}
+
+/* Time of the instance's next completion (+inf when idle).  The remaining
+ * virtual work is clamped at 0, so a completion never lies before t_last. */
+static double b_next(const binst* s, double beta) {
+  if (s->nact == 0) return INFINITY;
+  double rem = s->act[0].f - s->v;
+  if (rem < 0.0) rem = 0.0;
+  return s->t_last + rem * slowdown(beta, s->nact);
+}
+
+typedef struct {
+  const orc_point* pt;
+  binst *pre, *dec;
+  const int32_t *p, *o, *oh;
+  const int32_t* idec;    /* decode placements */
+  double *pf_end, *dec_end;
+  orc_stats* st;
+} bsim;
+
+/* Stand-alone (batch of one) service of request r in each stage: the serial
+ * model's service times. */
+static int64_t work_pre(const bsim* b, int64_t r) { return b->pt->pre_base_ns + (int64_t)b->p[r] * b->pt->pre_tok_ns; }
+static int64_t work_dec(const bsim* b, int64_t r) { return (int64_t)(b->o[r] - 1) * b->pt->dec_tok_ns; }
+
+/* Process every event at or before time T in time order (completions before
+ * transfer landings at equal times, lower instance first, prefill pool
+ * before decode pool), then bring every instance's virtual time to T
+ * (skipped for T = +inf, the final drain). */
+static int b_run_to(bsim* b, double T) {
+  const int32_t P = b->pt->n_prefill, D = b->pt->n_decode;
+  for (;;) {
+    double te = INFINITY;
+    int32_t k = -1;
+    int landing = 0;
+    for (int32_t j = 0; j < P + D; ++j) {
+      const double tc = j < P ? b_next(&b->pre[j], b->pt->beta_pre) : b_next(&b->dec[j - P], b->pt->beta_dec);
+      if (tc < te) {
+        te = tc;
+        k = j;
+      }
+    }
+    for (int32_t d = 0; d < D; ++d)
+      if (b->dec[d].nwait > 0 && b->dec[d].wait[0].t < te) {
+        te = b->dec[d].wait[0].t;
+        k = P + d;
+        landing = 1;
+      }
+    if (k < 0 || te > T) break;
+    if (!landing) {
+      /* every member sharing the smallest finish virtual time leaves */
+      const int is_pre = k < P;
+      binst* s = is_pre ? &b->pre[k] : &b->dec[k - P];
+      const double fmin = s->act[0].f;
+      s->v = fmin;
+      s->t_last = te;
+      int64_t m = 0;
+      while (m < s->nact && s->act[m].f == fmin) m++;
+      for (int64_t i = 0; i < m; ++i) {
+        const int64_t r = s->act[i].r;
+        s->queue -= 1;
+        if (is_pre) {
+          s->kv -= b->p[r];
+          s->pend -= b->p[r];
+          b->pf_end[r] = te;
+          b->st->retired_pre++;
+          /* the KV leaves for the decode instance and lands a transfer later */
+          if (wait_insert(&b->dec[b->idec[r]], te + (double)((int64_t)b->p[r] * b->pt->xfer_tok_ns), r)) return -2;
+        } else {
+          s->kv -= (int64_t)b->p[r] + b->o[r];
+          s->pend -= b->oh[r];
+          b->dec_end[r] = te;
+          b->st->retired_dec++;
+        }
+        if (s->queue < 0 || s->kv < 0 || s->pend < 0) b->st->violations++;
+      }
+      for (int64_t i = m; i < s->nact; ++i) s->act[i - m] = s->act[i];
+      s->nact -= m;
+    } else {
+      /* a KV lands: its request joins the decode batch */
+      binst* s = &b->dec[k - P];
+      const int64_t r = s->wait[0].r;
+      for (int64_t i = 1; i < s->nwait; ++i) s->wait[i - 1] = s->wait[i];
+      s->nwait--;
+      b_advance(s, b->pt->beta_dec, te);
+      s->owed_wait -= work_dec(b, r);
+      if (batch_insert(s, s->v + (double)work_dec(b, r), r)) return -2;
+    }
+  }
+  if (T < INFINITY) {
+    for (int32_t j = 0; j < P; ++j) b_advance(&b->pre[j], b->pt->beta_pre, T);
+    for (int32_t d = 0; d < D; ++d) b_advance(&b->dec[d], b->pt->beta_dec, T);
+  }
+  return 0;
+}
+
+/* Features of one pool.  Clock backlog: the stand-alone work (ns) the
+ * instance still owes, the batch's remaining virtual work summed in batch
+ * order plus, on a decode instance, the whole work of the requests routed
+ * there that have not joined (an exact integer), in seconds.  Ledger
+ * backlog: as in the serial model. */
+static void batched_features(const bsim* b, int32_t pool, float* backlog, int64_t* queue, int64_t* kv) {
+  const orc_point* pt = b->pt;
+  const int32_t n = pool == ORC_PREFILL ? pt->n_prefill : pt->n_decode;
+  for (int32_t j = 0; j < n; ++j) {
+    const binst* s = pool == ORC_PREFILL ? &b->pre[j] : &b->dec[j];
+    queue[j] = s->queue;
+    kv[j] = s->kv;
+    if (pt->backlog_mode == ORC_BACKLOG_TRUE) {
+      double w = 0.0;
+      for (int64_t i = 0; i < s->nact; ++i) {
+        const double rem = s->act[i].f - s->v;
+        w += rem < 0.0 ? 0.0 : rem; /* clamped as in b_next */
+      }
+      w += (double)s->owed_wait;
+      backlog[j] = (float)w * 1e-9f;
+    } else {
+      backlog[j] = ledger_backlog(pt, pool, s->queue, s->pend);
+    }
+  }
+}
+
+static void free_binst(binst* a, int32_t n) {
+  if (!a) return;
+  for (int32_t j = 0; j < n; ++j) {
+    free(a[j].act);
+    free(a[j].wait);
+  }
+  free(a);
+}
+
+int orc_sim_replica_batched(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
+                            const int32_t* prompt_len, const int32_t* out_len, const int32_t* pred_out_len,
+                            const uint8_t* slo_class, const uint32_t* sample_bits, const int32_t* follow_pre,
+                            const int32_t* follow_dec, double tie_rel, int32_t* i_pre, int32_t* i_dec,
+                            int64_t* ttft_ns, int64_t* span_ns, orc_stats* st) {
+  if (!pt || !st || n < 0) return -1;
+  if (pt->n_prefill < 1 || pt->n_decode < 1 || pt->n_classes < 1 || pt->n_classes > ORC_MAX_CLASSES ||
+      pt->kv_cap_pre < 1 || pt->kv_cap_dec < 1 || !(pt->beta_pre >= 0.0) || !(pt->beta_dec >= 0.0) ||
+      !isfinite(pt->beta_pre) || !isfinite(pt->beta_dec))
+    return -1;
+  if (pt->policy == ORC_LENGTH_THRESHOLD && pt->len_threshold < 1) return -1;
+  if (n > 0 && (!arrival_ns || !prompt_len || !out_len || !pred_out_len || !slo_class || !i_pre || !i_dec ||
+                !ttft_ns || !span_ns))
+    return -1;
+  if (pt->policy == ORC_LEARNED_SAMPLED && n > 0 && !sample_bits) return -1;
+  memset(st, 0, sizeof *st);
+  st->first_mismatch = -1;
+  const int32_t P = pt->n_prefill, D = pt->n_decode;
+  const int32_t N = P > D ? P : D;
+  bsim b;
+  memset(&b, 0, sizeof b);
+  b.pt = pt;
+  b.p = prompt_len;
+  b.o = out_len;
+  b.oh = pred_out_len;
+  b.idec = i_dec;
+  b.st = st;
+  b.pre = (binst*)calloc((size_t)P, sizeof(binst));
+  b.dec = (binst*)calloc((size_t)D, sizeof(binst));
+  b.pf_end = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+  b.dec_end = (double*)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+  float* f_backlog = (float*)calloc((size_t)N, sizeof(float));
+  int64_t* f_queue = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+  int64_t* f_kv = (int64_t*)calloc((size_t)N, sizeof(int64_t));
+  float* cost_pre = (float*)calloc((size_t)P, sizeof(float));
+  float* cost_dec = (float*)calloc((size_t)D, sizeof(float));
+  int rc = 0;
+  if (!b.pre || !b.dec || !b.pf_end || !b.dec_end || !f_backlog || !f_queue || !f_kv || !cost_pre || !cost_dec) {
+    rc = -2;
+    goto done;
+  }
+
+  int64_t last_arrival = 0;
+  int have_arrival = 0;
+  for (int64_t r = 0; r < n; ++r) {
+    const int64_t now = arrival_ns[r];
+    const int32_t p = prompt_len[r], o = out_len[r], oh = pred_out_len[r];
+    const uint8_t c = slo_class[r];
+    /* the serial model's data checks */
+    if (p < 1 || o < 1 || oh < 1 || (int64_t)p + o > INT32_MAX || (int64_t)p + oh > INT32_MAX ||
+        c >= pt->n_classes || now < 0 || (have_arrival && now < last_arrival)) {
+      st->invalid++;
+      i_pre[r] = i_dec[r] = -1;
+      continue;
+    }
+    last_arrival = now;
+    have_arrival = 1;
+
+    /* 1. every completion and transfer landing up to the arrival */
+    if ((rc = b_run_to(&b, (double)now)) != 0) goto done;
+
+    /* 2. each pool's argmin on that state */
+    int tie, close;
+    int32_t cand_pre[2], cand_dec[2];
+    const uint32_t* w = sample_bits ? sample_bits + 4 * r : NULL;
+    batched_features(&b, ORC_PREFILL, f_backlog, f_queue, f_kv);
+    int32_t ip = choose(pt, ORC_PREFILL, P, r, f_backlog, f_queue, f_kv, p, oh, c, w, tie_rel, cost_pre, cand_pre,
+                        &tie, &close);
+    st->tie_pre += tie;
+    st->close_pre += close;
+    batched_features(&b, ORC_DECODE, f_backlog, f_queue, f_kv);
+    int32_t id = choose(pt, ORC_DECODE, D, r, f_backlog, f_queue, f_kv, p, oh, c, w ? w + 2 : NULL, tie_rel,
+                        cost_dec, cand_dec, &tie, &close);
+    st->tie_dec += tie;
+    st->close_dec += close;
+    if (follow_pre)
+      ip = follow(pt, ip, follow_pre[r], P, cost_pre, cand_pre, tie_rel, &st->near_tie_pre, &st->mismatch_pre,
+                  &st->first_mismatch, r);
+    if (follow_dec)
+      id = follow(pt, id, follow_dec[r], D, cost_dec, cand_dec, tie_rel, &st->near_tie_dec, &st->mismatch_dec,
+                  &st->first_mismatch, r);
+    i_pre[r] = ip;
+    i_dec[r] = id;
+
+    /* 3. admission: the prefill batch takes the request now; the decode
+     * instance holds its cache and counts it from now, and takes it into its
+     * batch when its KV lands */
+    binst* a = &b.pre[ip];
+    if (batch_insert(a, a->v + (double)work_pre(&b, r), r)) {
+      rc = -2;
+      goto done;
+    }
+    a->queue += 1;
+    a->kv += p;
+    a->pend += p;
+    if (a->kv > pt->kv_cap_pre) st->over_cap_pre++;
+    if (a->queue > st->max_queue_pre) st->max_queue_pre = a->queue;
+    binst* d = &b.dec[id];
+    d->owed_wait += work_dec(&b, r);
+    d->queue += 1;
+    d->kv += (int64_t)p + o;
+    d->pend += oh;
+    if (d->kv > pt->kv_cap_dec) st->over_cap_dec++;
+    if (d->queue > st->max_queue_dec) st->max_queue_dec = d->queue;
+  }
+  for (int32_t j = 0; j < P; ++j) st->end_inflight_pre += b.pre[j].queue;
+  for (int32_t j = 0; j < D; ++j) st->end_inflight_dec += b.dec[j].queue;
+  /* 4. drain: everything in flight finishes; then every count is zero */
+  {
+    const int64_t kept_pre = st->retired_pre, kept_dec = st->retired_dec;
+    if ((rc = b_run_to(&b, INFINITY)) != 0) goto done;
+    st->retired_pre = kept_pre;
+    st->retired_dec = kept_dec;
+  }
+  for (int32_t j = 0; j < P; ++j)
+    if (b.pre[j].queue || b.pre[j].kv || b.pre[j].pend || b.pre[j].nact) st->violations++;
+  for (int32_t j = 0; j < D; ++j)
+    if (b.dec[j].queue || b.dec[j].kv || b.dec[j].pend || b.dec[j].nact || b.dec[j].nwait || b.dec[j].owed_wait)
+      st->violations++;
+  /* 5. outcomes, rounded to whole ns (nearest, ties to even) */
+  for (int64_t r = 0; r < n; ++r) {
+    if (i_pre[r] < 0) {
+      ttft_ns[r] = span_ns[r] = -1;
+      continue;
+    }
+    if (!(b.pf_end[r] >= (double)arrival_ns[r]) || !(b.dec_end[r] >= b.pf_end[r])) st->violations++;
+    ttft_ns[r] = llrint(b.pf_end[r] - (double)arrival_ns[r]);
+    span_ns[r] = llrint(b.dec_end[r] - b.pf_end[r]);
+  }
+
+done:
+  free_binst(b.pre, P);
+  free_binst(b.dec, D);
+  free(b.pf_end);
+  free(b.dec_end);
+  free(f_backlog);
+  free(f_queue);
+  free(f_kv);
+  free(cost_pre);
+  free(cost_dec);
+  return rc;
 }

@@ -18,13 +18,17 @@
  *                       optionally in "follow" mode, where it adopts
  *                       externally supplied placements and accounts every
  *                       divergence from its own choice;
+ *   - orc_sim_replica_batched: the same replica under continuous batching
+ *                       in both stages (processor sharing with a
+ *                       batch-dependent slowdown);
  *   - orc_goodput:      fraction of a replica's requests meeting both the
  *                       TTFT and the TPOT target of their class.
  *
  * Every floating-point step is evaluated in float32 in the order the cost
  * equation is written, left to right, one rounding per operation (the
  * library is built with -ffp-contract=off, so no fused multiply-add).
- * All simulated times are int64 nanoseconds.
+ * Simulated times are int64 nanoseconds in the serial model and float64
+ * nanoseconds inside the batched one.
  */
 #ifndef RT_ORACLE_H
 #define RT_ORACLE_H
@@ -64,7 +68,11 @@ typedef struct {
   int64_t kv_cap_pre, kv_cap_dec;
   int64_t slo_ttft_ns[ORC_MAX_CLASSES], slo_tpot_ns[ORC_MAX_CLASSES];
   int32_t len_threshold; /* ORC_LENGTH_THRESHOLD only */
+  int32_t service;       /* ORC_SERIAL or ORC_BATCHED (orc_sim_replica_batched) */
+  double beta_pre, beta_dec; /* ORC_BATCHED: per-request slowdown per extra batch member */
 } orc_point;
+
+enum { ORC_SERIAL = 0, ORC_BATCHED = 1 };
 
 typedef struct {
   int64_t invalid;                   /* requests rejected by the data checks   */
@@ -126,6 +134,40 @@ int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
                     const int32_t* follow_pre, const int32_t* follow_dec, double tie_rel,
                     int32_t* i_pre, int32_t* i_dec, int64_t* ttft_ns, int64_t* span_ns,
                     orc_stats* st);
+
+/* The same replica under continuous batching in both stages (the service
+ * model Section VI adds to the serial one): every instance serves all its
+ * admitted requests at once, each at 1 / (1 + beta * (b - 1)) of its
+ * stand-alone speed while b requests share the instance (beta_pre for
+ * prefill, beta_dec for decode, finite and >= 0; a batch of one runs at full
+ * speed, so the model reduces to the serial one wherever requests never
+ * overlap).  A request's stand-alone work is its serial service time.  It
+ * joins its prefill instance's batch at its arrival and its decode
+ * instance's batch when its KV lands there (prefill end + transfer); it holds
+ * cache and ledger tokens and counts in the queue of both instances from its
+ * admission to the end of that stage.
+ * Each instance keeps a virtual clock v (stand-alone service received by
+ * every member since the instance's start), advanced by dt / (1 + beta (b-1))
+ * at each of its events, and a batch of members sorted by finish virtual
+ * time f = v at joining + work (then by request index); its next completion
+ * lies at t_last + max(f_min - v, 0) * (1 + beta (b - 1)), and every member
+ * with f == f_min leaves then.
+ * Clock backlog is the stand-alone work the instance still owes, in
+ * seconds: the sum over its batch, in batch order, of max(f - v, 0), plus (decode)
+ * the int64 sum of the decode work of the requests routed there that have
+ * not joined; ledger backlog as in the serial model.
+ * Times are float64 ns, events at equal times in the order: completions,
+ * then KV landings, then the arrival being routed; the lower-numbered
+ * instance first (prefill pool before decode pool), landings in request
+ * order.  ttft and span are rounded to whole ns (nearest, ties to even).
+ * Same arguments and outputs as orc_sim_replica; follow mode and
+ * sample_bits as there.  Returns -1 also for a negative or non-finite
+ * beta. */
+int orc_sim_replica_batched(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
+                            const int32_t* prompt_len, const int32_t* out_len, const int32_t* pred_out_len,
+                            const uint8_t* slo_class, const uint32_t* sample_bits, const int32_t* follow_pre,
+                            const int32_t* follow_dec, double tie_rel, int32_t* i_pre, int32_t* i_dec,
+                            int64_t* ttft_ns, int64_t* span_ns, orc_stats* st);
 
 /* Number of requests meeting both SLO targets of their class; *goodput is
  * that count over n (0 when n == 0). */

@@ -75,6 +75,13 @@ A40_PHYSICS = dict(
 )
 
 
+# Continuous batching (Section VI): the measured decode curve is nearly flat,
+# a batch of eight costing each request 2.9 % more per token, i.e. a factor
+# 1 + beta (b - 1) with beta = 0.029 / 7 per extra batch member.  The paper
+# gives no prefill curve; the same beta for prefill is this build's reading.
+BATCH_BETA = 0.029 / 7
+
+
 def xfer_tok_ns(kv_bytes_per_token: int, link_bytes_per_s: float = LINK_BYTES_PER_S) -> int:
     """KV transfer delay per prompt token in ns (bytes/token over the link)."""
     return int(round(kv_bytes_per_token / link_bytes_per_s * 1e9))
@@ -130,12 +137,19 @@ def make_point(
     sigma: Optional[Sequence[float]] = None,
     link_bytes_per_s: float = LINK_BYTES_PER_S,
     len_threshold: int = 256,
+    service: str = "serial",
+    beta_pre: float = None,
+    beta_dec: float = None,
 ) -> Dict:
     """One parameter point: pool shape, router constants, physics and SLOs.
 
     Router constants are the priced view (float32 seconds); physics is the
     true service model (int64 ns).  ``tau_*_scale`` multiplies the router's
     per-token prices relative to the physics (1.0 = calibrated, Section III-B).
+    ``service`` is "serial" (one request at a time per instance) or "batched"
+    (continuous batching in both stages: each of b requests sharing an
+    instance runs at 1 / (1 + beta (b - 1)) of its stand-alone speed);
+    both betas default to BATCH_BETA, the measured decode curve of Section VI.
     """
     ph = dict(SIM_PHYSICS if physics is None else physics)
     ttft, tpot = slo_targets(ph["dec_tok_ns"], n_classes)
@@ -163,6 +177,9 @@ def make_point(
         kv_cap_dec=int(kv_cap),
         slo_ttft_ns=[int(v) for v in ttft],
         slo_tpot_ns=[int(v) for v in tpot],
+        service=service,
+        beta_pre=float(BATCH_BETA if beta_pre is None else beta_pre),
+        beta_dec=float(BATCH_BETA if beta_dec is None else beta_dec),
     )
 
 
