@@ -46,6 +46,10 @@ def _workload(name):
         return W.paper_cluster()
     if name == "cluster_sampled":
         return W.paper_cluster(policy="learned_sampled")
+    if name == "cluster_batched":
+        return W.paper_cluster(service="batched")
+    if name == "cluster_batched_wide":
+        return W.paper_cluster(n_replicas=65536, requests=2000, service="batched")
     if name == "sweep":
         return W.param_sweep()
     if name == "large":
@@ -63,7 +67,7 @@ def _source_hash(files):
 
 SIM_SOURCES = ["paper_2609_16206_amd/csrc/" + f for f in (
     "seg_kernel.h", "wseg_kernel.h", "seg_true.hip", "seg_proxy.hip", "seg_base.hip", "seg_true_s.hip", "seg_proxy_s.hip", "seg_classes.hip",
-    "lane_ops.h", "rt_internal.h")]
+    "lane_ops.h", "rt_internal.h", "bat_kernel.hip")]
 SCORE_SOURCES = ["paper_2609_16206_amd/csrc/score_kernel.hip", "paper_2609_16206_amd/csrc/rt_internal.h"]
 
 
@@ -161,7 +165,9 @@ def bench_sim(args):
         roof = dict(bound="alu", achieved=alg_ops / kernel_s / 1e12, peak=ALU_PEAK / 1e12, unit="Tlane-op/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = _traffic("sim", args.workload, SIM_SOURCES)
-    roof["kernel"] = "rt::seg::seg_kernel / wseg_kernel (every class one rt_sim_run_replicas call launches)"
+    batched = any(p.get("service") == "batched" for p in wl.points)
+    roof["kernel"] = ("rt::bat::bat_kernel" if batched else
+                      "rt::seg::seg_kernel / wseg_kernel (every class one rt_sim_run_replicas call launches)")
     roof["kernel_ms"] = kernel_s * 1e3
     roof["alg_bytes"] = alg_bytes
     roof["alg_lane_ops"] = alg_ops
@@ -173,7 +179,7 @@ def bench_sim(args):
                config=dict(workload=wl.name, replicas=wl.n_replicas, requests_per_replica=wl.requests,
                            points=len(wl.points), prefill=pt["n_prefill"] if len(wl.points) == 1 else "mixed",
                            decode=pt["n_decode"] if len(wl.points) == 1 else "mixed",
-                           policy=pt["policy"], backlog=pt["backlog_mode"]),
+                           policy=pt["policy"], backlog=pt["backlog_mode"], service=pt.get("service", "serial")),
                pairs_per_s=n_pairs * args.steps / dt, requests=n_req, pairs=n_pairs, mean_goodput=mean_goodput,
                data_flags=flags, roofline=roof, trace_gen_s=t_gen)
     if not args.no_cpu_baseline:
@@ -244,7 +250,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="cluster",
-                    choices=["tiny", "cluster", "cluster_sampled", "sweep", "large", "scorer"])
+                    choices=["tiny", "cluster", "cluster_sampled", "cluster_batched", "cluster_batched_wide", "sweep",
+                             "large", "scorer"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",

@@ -85,6 +85,15 @@ typedef enum {
 
 typedef enum { RT_POOL_PREFILL = 0, RT_POOL_DECODE = 1 } rt_pool;
 
+typedef enum {
+  RT_SERVICE_SERIAL = 0,  /* one request at a time per instance, in admission order
+                             (the serial-service model of Section III-D / VI)        */
+  RT_SERVICE_BATCHED = 1  /* continuous batching in both stages (the model Section VI
+                             adds): every admitted request is served at once, each at
+                             1 / (1 + beta (b - 1)) of its stand-alone speed while b
+                             requests share the instance (see rt_sim_run_replicas)  */
+} rt_service;
+
 #define RT_MAX_CLASSES 8
 #define RT_MAX_POOL 1024 /* instances per pool */
 
@@ -119,6 +128,15 @@ typedef struct {
   int32_t len_threshold;       /* RT_POLICY_LENGTH_THRESHOLD: predicted output
                                   tokens at which a request counts as long
                                   (>= 1); unread by the other policies      */
+  int32_t service;             /* rt_service                              */
+  double beta_pre, beta_dec;   /* RT_SERVICE_BATCHED: slowdown per extra
+                                  batch member in prefill / decode, finite
+                                  and >= 0 (the measured decode curve of
+                                  Section VI: 0.029 / 7)                    */
+  int32_t batch_cap;           /* RT_SERVICE_BATCHED: room per instance for
+                                  batch members and for KV transfers in
+                                  flight; 0 = 256, else a power of two in
+                                  [2, 65536]                               */
   int32_t reserved;            /* set to 0                                */
 } rt_point;
 
@@ -189,10 +207,35 @@ typedef struct {
  * D == 1 both parts are instance 0), a request with o^_r >= len_threshold
  * goes to the least loaded instance of the upper part, any other request to
  * the least loaded of the lower part.
+ * A point with service RT_SERVICE_BATCHED changes how instances serve, not
+ * how the router scores (the cost equation and every policy read the same
+ * features).  Its request joins its prefill instance's batch at its arrival
+ * and its decode instance's batch when its KV lands there (prefill end +
+ * transfer); while b requests share an instance, each receives stand-alone
+ * service at 1 / (1 + beta (b - 1)) of full speed (beta_pre, beta_dec), and
+ * it leaves when it has received its stand-alone work (the serial service
+ * time).  It holds its cache and ledger tokens and counts in the queue of
+ * both instances from its admission to the end of each stage, as in the
+ * serial model.  Each instance keeps a virtual clock v (stand-alone service
+ * received by each member), advanced by dt / (1 + beta (b - 1)) at each of
+ * its events; members are ordered by finish virtual time f = v at joining +
+ * work, then request index; the next completion lies at
+ * t_last + max(f_min - v, 0) (1 + beta (b - 1)), and every member with
+ * f == f_min leaves then.  Clock backlog is the stand-alone work still owed:
+ * the sum in member order of max(f - v, 0), plus on a decode instance the
+ * decode work of requests routed there that have not joined (an exact
+ * integer sum, added last), in seconds; ledger backlog is unchanged.  Times
+ * are float64 ns; at equal times completions come first, then KV landings,
+ * then the arrival being routed.  TTFT and decode span are rounded to whole
+ * ns (nearest, ties to even).  An instance holds at most batch_cap members
+ * and batch_cap KV transfers in flight; a replica that would exceed either
+ * stops there (its outputs are not valid) and sets flag bit 3.
  * The call reads offsets and param_point back to the host to plan the launch
  * (it synchronizes `hip_stream` for that), validates them (RT_EINVAL), then
  * enqueues the simulation on `hip_stream` and returns.  Scratch memory grows
- * with n_requests (80 bytes per request) and is owned by `sim`. */
+ * with n_requests (80 bytes per request), and for batched replicas with
+ * (P + D) x (64 + 32 batch_cap) bytes per replica (largest P + D and
+ * batch_cap of the call's batched points); it is owned by `sim`. */
 rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* out, void* hip_stream);
 
 /* Per-replica goodput: the fraction of the replica's requests that meet both
@@ -212,7 +255,9 @@ rt_status rt_goodput(const rt_sim* sim, const rt_trace* trace, const rt_sim_out*
  *          inconsistent (its goodput is 0 and its met count -1);
  *   bit 2: a simulated time reached 2^52 ns (about 52 days), beyond which
  *          the kernels' exact integer arithmetic no longer holds (the
- *          outputs of such a run are not valid). */
+ *          outputs of such a run are not valid);
+ *   bit 3: a replica of a batched point outgrew its point's batch_cap (its
+ *          outputs are not valid; run it again with a larger batch_cap). */
 rt_status rt_sim_data_status(rt_sim* sim, void* hip_stream, uint32_t* flags);
 
 /* Measurement hook.  rt_sim_timing(sim, 1) resets the totals and makes every

@@ -43,6 +43,8 @@ struct DeviceScope {
 bool finite_nonneg(float x) { return std::isfinite(x) && x >= 0.0f; }
 
 constexpr int64_t kMaxNs = int64_t(1) << 40;
+constexpr int32_t kMaxBatchCap = 65536;
+constexpr int32_t kDefaultBatchCap = 256;
 constexpr int kSimds = 256 * 4;  // MI355X: 256 compute units x 4 SIMDs
 
 std::string check_point(const rt_point& p) {
@@ -52,6 +54,14 @@ std::string check_point(const rt_point& p) {
   if (p.policy < RT_POLICY_LEARNED || p.policy > RT_POLICY_LENGTH_THRESHOLD) return "unknown policy";
   if (p.policy == RT_POLICY_LENGTH_THRESHOLD && p.len_threshold < 1) return "len_threshold must be >= 1";
   if (p.backlog_mode != RT_BACKLOG_TRUE && p.backlog_mode != RT_BACKLOG_PROXY) return "unknown backlog_mode";
+  if (p.service != RT_SERVICE_SERIAL && p.service != RT_SERVICE_BATCHED) return "unknown service";
+  if (p.service == RT_SERVICE_BATCHED) {
+    if (!std::isfinite(p.beta_pre) || !std::isfinite(p.beta_dec) || p.beta_pre < 0.0 || p.beta_dec < 0.0)
+      return "beta_pre and beta_dec must be finite and >= 0";
+    const int32_t c = p.batch_cap;
+    if (c != 0 && (c < 2 || c > kMaxBatchCap || (c & (c - 1)) != 0))
+      return "batch_cap must be 0 or a power of two in [2, 65536]";
+  }
   const rt_router_params& r = p.router;
   const float f[] = {r.w_b, r.w_s, r.w_q, r.rho, r.tau_pre_s, r.tau_dec_s, r.pre_base_s};
   for (float x : f)
@@ -78,6 +88,10 @@ rt::DevPoint to_dev(const rt_point& p) {
   d.policy = p.policy;
   d.len_thr = p.len_threshold;
   d.mode = p.backlog_mode;
+  d.service = p.service;
+  d.batch_cap = p.batch_cap == 0 ? kDefaultBatchCap : p.batch_cap;
+  d.beta_pre = p.beta_pre;
+  d.beta_dec = p.beta_dec;
   // Adding +0.0f turns a -0.0f weight into +0.0f (and changes nothing else):
   // with every factor then +0 or positive, no cost is -0 and the kernels can
   // order costs by their bit patterns without a zero test.
@@ -112,11 +126,15 @@ int point_mode(const rt_point& p) {
   return rt::kModeBase;
 }
 
-// Does kernel class c hold both pools of point p?  A one-wave segment class
+// Does kernel class c hold both pools of point p?  A batched-service point
+// takes the batched class, any other point a serial one.  A one-wave segment class
 // of the point's mode needs ceil(P / M) prefill lanes and ceil(D / M) decode
 // lanes within its S; a multi-wave one needs every wave's share of both
 // within 64 lanes.
 bool class_fits(const rt::SimClass& c, const rt_point& p) {
+  // the batched service model has one class of its own
+  if ((c.kind == rt::kBat) != (p.service == RT_SERVICE_BATCHED)) return false;
+  if (c.kind == rt::kBat) return true;
   if (c.kind == rt::kSeg) {
     if (c.mode != point_mode(p)) return false;
     const int lanes = (p.n_prefill + c.MP - 1) / c.MP + (p.n_decode + c.MD - 1) / c.MD;
@@ -155,6 +173,8 @@ struct rt_sim {
   uint32_t* d_flag = nullptr;
   char* d_scratch = nullptr;
   size_t scratch_bytes = 0;
+  char* d_bscratch = nullptr;  // the batched class's state and rings
+  size_t bscratch_bytes = 0;
   int32_t* d_work = nullptr;
   size_t work_cap = 0;
   int32_t* h_work = nullptr;  // pinned staging for the work list
@@ -248,6 +268,7 @@ rt_status rt_sim_destroy(rt_sim* sim) {
   if (sim->d_points) (void)hipFree(sim->d_points);
   if (sim->d_flag) (void)hipFree(sim->d_flag);
   if (sim->d_scratch) (void)hipFree(sim->d_scratch);
+  if (sim->d_bscratch) (void)hipFree(sim->d_bscratch);
   if (sim->d_work) (void)hipFree(sim->d_work);
   if (sim->h_work) (void)hipHostFree(sim->h_work);
   if (sim->upload_done) (void)hipEventDestroy(sim->upload_done);
@@ -352,12 +373,21 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
     });
 
   hipError_t e;
-  // Scratch: the dummy records, then the successor records (kRecStride
-  // bytes each).
+  // Scratch of the serial classes: the dummy records, then the successor
+  // records (kRecStride bytes each).
+  bool any_serial = false;
+  int bat_class = -1;
+  for (int c = 0; c < ncls; ++c) {
+    if (buckets[c].empty()) continue;
+    if (rt::sim_class(c).kind == rt::kBat)
+      bat_class = c;
+    else
+      any_serial = true;
+  }
   const size_t nreq = (size_t)trace->n_requests;
   const size_t dummy_bytes = (size_t)rt::kDummyRecords * rt::kRecStride;
   static_assert(((size_t)rt::kDummyRecords * rt::kRecStride) % 256 == 0, "records stay 256-byte aligned");
-  const size_t need = nreq * rt::kRecStride + dummy_bytes + 256;
+  const size_t need = any_serial ? nreq * rt::kRecStride + dummy_bytes + 256 : 0;
   if (need > sim->scratch_bytes) {
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
     if (sim->d_scratch) (void)hipFree(sim->d_scratch);
@@ -365,6 +395,29 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
     sim->scratch_bytes = 0;
     if ((e = hipMalloc(&sim->d_scratch, need)) != hipSuccess) return hip_fail(e, "hipMalloc(scratch)");
     sim->scratch_bytes = need;
+  }
+  // Scratch of the batched class: per-instance state and two rings per
+  // instance for every lane, sized by the largest pool and capacity among its
+  // replicas' points.
+  rt::BatScratch bs{};
+  if (bat_class >= 0) {
+    int32_t NI = 1, C = 2;
+    for (int32_t r : buckets[bat_class]) {
+      const rt_point& q = sim->points[pp[r]];
+      NI = std::max(NI, q.n_prefill + q.n_decode);
+      C = std::max(C, q.batch_cap == 0 ? kDefaultBatchCap : q.batch_cap);
+    }
+    const int64_t S = (int64_t)buckets[bat_class].size();
+    const size_t bneed = rt::bat_scratch_bytes(S, NI, C) + 256;
+    if (bneed > sim->bscratch_bytes) {
+      if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+      if (sim->d_bscratch) (void)hipFree(sim->d_bscratch);
+      sim->d_bscratch = nullptr;
+      sim->bscratch_bytes = 0;
+      if ((e = hipMalloc(&sim->d_bscratch, bneed)) != hipSuccess) return hip_fail(e, "hipMalloc(batched scratch)");
+      sim->bscratch_bytes = bneed;
+    }
+    bs = rt::bat_scratch_carve(sim->d_bscratch, S, NI, C);
   }
   if ((size_t)n > sim->work_cap) {
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
@@ -416,7 +469,7 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   a.i_dec = out->i_dec;
   a.ttft = out->ttft_ns;
   a.span = out->decode_span_ns;
-  a.rec = sc + dummy_bytes;
+  a.rec = sc ? sc + dummy_bytes : nullptr;
   a.flag = sim->d_flag;
   if (sim->timing) {
     if ((st = collect_timing(sim)) != RT_OK) return st;
@@ -454,7 +507,8 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
       where = sim->lanes[k];
       if ((e = hipStreamWaitEvent(where, sim->fork, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
-    if ((e = rt::launch_sim(rt::sim_class(c), a, where)) != hipSuccess) return hip_fail(e, "launch(sim)");
+    e = rt::sim_class(c).kind == rt::kBat ? rt::launch_bat(a, bs, where) : rt::launch_sim(rt::sim_class(c), a, where);
+    if (e != hipSuccess) return hip_fail(e, "launch(sim)");
     if (act.size() > 1 && (e = hipEventRecord(sim->joins[k], where)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   }
   // The joins go in after every launch: streams share the device's few

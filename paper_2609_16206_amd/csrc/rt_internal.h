@@ -12,7 +12,8 @@ constexpr int kMaxClasses = 8;
 // One parameter point as the kernels read it: the public rt_point plus
 // host-computed constants (reciprocal cache capacities).
 struct DevPoint {
-  int32_t P, D, n_classes, policy, mode, len_thr, pad0[2];
+  int32_t P, D, n_classes, policy, mode, len_thr;
+  int32_t service, batch_cap;  // rt_service; ring capacity (power of two)
   float w_b, w_s, w_q, rho;
   float tau_pre, tau_dec, pre_base;
   float inv_cap_pre, inv_cap_dec;  // 1.0f / (float)capacity, rounded once
@@ -20,9 +21,10 @@ struct DevPoint {
   float sigma[kMaxClasses];
   int64_t pre_base_ns, pre_tok_ns, dec_tok_ns, xfer_tok_ns;
   int64_t slo_ttft[kMaxClasses], slo_tpot[kMaxClasses];
+  double beta_pre, beta_dec;  // batched service: slowdown per extra member
 };
 
-enum : uint32_t { kFlagRejected = 1u, kFlagBadTrace = 2u, kFlagTimeRange = 4u };
+enum : uint32_t { kFlagRejected = 1u, kFlagBadTrace = 2u, kFlagTimeRange = 4u, kFlagBatchCap = 8u };
 
 // rt_policy values as the kernels read them from DevPoint::policy.
 enum : int32_t {
@@ -77,7 +79,8 @@ constexpr int kDummyRecords = 1024;  // a power of two
 // backlog, ledger backlog, or a baseline policy; the two learned ones also
 // over two sampled candidates per pool).  kWseg: the same for one replica
 // per workgroup of S / 64 waves, instances dealt round-robin over the waves.
-enum SimKind { kSeg = 0, kWseg = 1 };
+// kBat: the continuous-batching service model, one replica per lane.
+enum SimKind { kSeg = 0, kWseg = 1, kBat = 2 };
 enum SimMode { kModeTrue = 0, kModeProxy = 1, kModeBase = 2, kModeTrueSampled = 3, kModeProxySampled = 4 };
 constexpr bool mode_ledger(int m) { return m == kModeProxy || m == kModeProxySampled; }  // proxy backlog
 constexpr bool mode_sampled(int m) { return m == kModeTrueSampled || m == kModeProxySampled; }
@@ -91,6 +94,26 @@ struct SimClass {
 hipError_t launch_sim(const SimClass& c, const SimArgs& a, hipStream_t stream);
 int sim_class_count();
 SimClass sim_class(int i);
+
+// Scratch of the continuous-batching kernel for S lanes, NI instance slots
+// per lane (the largest P + D of the launch) and ring capacity C (a power of
+// two).  Per-instance state is structure-of-arrays, element [j * S + lane]
+// (a wave reads 64 consecutive elements); the rings are per lane, contiguous,
+// 16 bytes an entry, entry [((lane * NI + j) * C + pos].
+struct BatScratch {
+  double *v, *tl, *kv, *pend, *owed;       // [NI][S]
+  int32_t *q, *nact, *head, *nw, *whead;   // [NI][S]
+  char* ring;   // batch members {f, request}, sorted by (f, request) from head
+  char* wring;  // KV transfers in flight {landing time, request}, sorted likewise
+  int64_t S;
+  int32_t NI, C;
+};
+
+// Bytes of BatScratch for S lanes, NI instance slots and capacity C, and the
+// carving of one allocation into it.
+size_t bat_scratch_bytes(int64_t S, int32_t NI, int32_t C);
+BatScratch bat_scratch_carve(char* base, int64_t S, int32_t NI, int32_t C);
+hipError_t launch_bat(const SimArgs& a, const BatScratch& b, hipStream_t stream);
 
 struct ScoreArgs {
   float w_b, w_s, w_q, rho, tau, inv_cap;

@@ -27,9 +27,12 @@ constexpr int kNumModes = (int)(sizeof(kModes) / sizeof(kModes[0]));
 
 }  // namespace
 
-int sim_class_count() { return (kNumShapes + kNumWide) * kNumModes; }
+// The one-wave and multi-wave classes of every mode, then the batched
+// service model's class (one replica per lane; its launch is launch_bat).
+int sim_class_count() { return (kNumShapes + kNumWide) * kNumModes + 1; }
 
 SimClass sim_class(int i) {
+  if (i == (kNumShapes + kNumWide) * kNumModes) return SimClass{kBat, 1, 1, 1, kModeTrue};
   if (i < kNumShapes * kNumModes) {
     const SegShape& e = kShapes[i % kNumShapes];
     return SimClass{kSeg, e.S, e.M, e.M, kModes[i / kNumShapes]};
@@ -40,6 +43,7 @@ SimClass sim_class(int i) {
 }
 
 hipError_t launch_sim(const SimClass& c, const SimArgs& a, hipStream_t stream) {
+  if (c.kind == kBat) return hipErrorInvalidValue;  // needs its scratch: launch_bat
   const bool w = c.kind == kWseg;
   const int S = w ? c.S / 64 : c.S;
   switch (c.mode) {

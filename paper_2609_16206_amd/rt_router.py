@@ -23,6 +23,7 @@ RT_OK, RT_EINVAL, RT_ENOMEM, RT_EDEVICE, RT_ERANGE, RT_EUNSUPPORTED, RT_EDATA = 
 RT_POLICY = {"learned": 0, "round_robin": 1, "least_loaded": 2, "learned_sampled": 3, "length_threshold": 4}
 RT_BACKLOG = {"true": 0, "proxy": 1}
 RT_POOL = {"prefill": 0, "decode": 1}
+RT_SERVICE = {"serial": 0, "batched": 1}
 RT_MAX_CLASSES = 8
 RT_MAX_POOL = 1024
 
@@ -51,7 +52,9 @@ class rt_physics(C.Structure):
 class rt_point(C.Structure):
     _fields_ = [("n_prefill", C.c_int32), ("n_decode", C.c_int32), ("n_classes", C.c_int32),
                 ("policy", C.c_int32), ("backlog_mode", C.c_int32), ("router", rt_router_params),
-                ("phys", rt_physics), ("len_threshold", C.c_int32), ("reserved", C.c_int32)]
+                ("phys", rt_physics), ("len_threshold", C.c_int32), ("service", C.c_int32),
+                ("beta_pre", C.c_double), ("beta_dec", C.c_double), ("batch_cap", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class rt_trace(C.Structure):
@@ -147,6 +150,11 @@ def point(d: Dict) -> rt_point:
         p.phys.slo_ttft_ns[i] = int(d["slo_ttft_ns"][i])
         p.phys.slo_tpot_ns[i] = int(d["slo_tpot_ns"][i])
     p.len_threshold = int(d.get("len_threshold", 1))
+    sv = d.get("service", "serial")
+    p.service = RT_SERVICE[sv] if isinstance(sv, str) else int(sv)
+    p.beta_pre = float(d.get("beta_pre", 0.0))
+    p.beta_dec = float(d.get("beta_dec", 0.0))
+    p.batch_cap = int(d.get("batch_cap", 0))
     p.reserved = 0
     return p
 

@@ -493,11 +493,13 @@ def tiny_sim(seed: int = 0) -> Workload:
 
 
 def paper_cluster(n_replicas: int = 4096, requests: int = 10_000, seed: int = 2,
-                  policy: str = "learned") -> Workload:
-    """2 prefill + 6 decode, mixed bursty MMPP (3 / 12 req/s, 20 s dwell)."""
+                  policy: str = "learned", service: str = "serial") -> Workload:
+    """2 prefill + 6 decode, mixed bursty MMPP (3 / 12 req/s, 20 s dwell);
+    ``service="batched"`` serves it under continuous batching (BATCH_BETA)."""
     tag = "" if policy == "learned" else "-" + policy.replace("_", "-")
+    tag += "" if service == "serial" else "-" + service
     return Workload(f"cluster-2p6d-mmpp-{n_replicas}x{requests}{tag}", seed, n_replicas, requests,
-                    [make_point(2, 6, n_classes=3, policy=policy)], [mixed_bursty()])
+                    [make_point(2, 6, n_classes=3, policy=policy, service=service)], [mixed_bursty()])
 
 
 SWEEP_WIDTHS = (3, 4, 6, 8, 16, 32, 64)

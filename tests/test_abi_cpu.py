@@ -40,7 +40,8 @@ def test_struct_layout_matches_header(rt, tmp_path):
     fields = {
         "rt_router_params": ["w_b", "tau_pre_s", "pre_base_s", "sigma"],
         "rt_physics": ["pre_base_ns", "kv_cap_dec", "slo_ttft_ns", "slo_tpot_ns"],
-        "rt_point": ["n_prefill", "backlog_mode", "router", "phys", "len_threshold", "reserved"],
+        "rt_point": ["n_prefill", "backlog_mode", "router", "phys", "len_threshold", "service", "beta_pre",
+                     "beta_dec", "batch_cap", "reserved"],
         "rt_trace": ["n_replicas", "n_requests", "offsets", "param_point", "slo_class", "sample_bits"],
         "rt_sim_out": ["i_pre", "decode_span_ns"],
     }
