@@ -166,7 +166,7 @@ def bench_sim(args):
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = _traffic("sim", args.workload, SIM_SOURCES)
     batched = any(p.get("service") == "batched" for p in wl.points)
-    roof["kernel"] = ("rt::bat::bat_kernel" if batched else
+    roof["kernel"] = ("rt::bat::bseg_kernel / bat_kernel (the batched classes the call launches)" if batched else
                       "rt::seg::seg_kernel / wseg_kernel (every class one rt_sim_run_replicas call launches)")
     roof["kernel_ms"] = kernel_s * 1e3
     roof["alg_bytes"] = alg_bytes

@@ -458,6 +458,9 @@ typedef struct {
 
 typedef struct {
   double v, t_last;  /* virtual time, valid at time t_last                  */
+  double rem;        /* stand-alone work the batch still owes (ns): + each
+                        joining member's work, - b * every virtual-time
+                        step, 0 once the batch empties                      */
   bmember* act;      /* the batch, sorted by (f, r)                          */
   int64_t nact, cap;
   bjoin* wait;       /* decode only: transfers in flight, sorted by (t, r)   */
@@ -505,10 +508,22 @@ static int wait_insert(binst* s, double t, int64_t r) {
   return 0;
 }
 
-/* Bring the instance's virtual time to time t, with no event in between. */
+/* Bring the instance's virtual time to time t, with no event in between:
+ * each of the b members receives dv of service. */
 static void b_advance(binst* s, double beta, double t) {
-  if (s->nact > 0) s->v += (t - s->t_last) / slowdown(beta, s->nact);
+  if (s->nact > 0) {
+    const double dv = (t - s->t_last) / slowdown(beta, s->nact);
+    s->v += dv;
+    s->rem -= (double)s->nact * dv;
+  }
   s->t_last = t;
+}
+
+/* A member joins with stand-alone work w. */
+static int b_join(binst* s, double w, int64_t r) {
+  if (batch_insert(s, s->v + w, r)) return -1;
+  s->rem += w;
+  return 0;
 }
 
 /* Time of the instance's next completion (+inf when idle).  The remaining
@@ -563,6 +578,7 @@ static int b_run_to(bsim* b, double T) {
       const int is_pre = k < P;
       binst* s = is_pre ? &b->pre[k] : &b->dec[k - P];
       const double fmin = s->act[0].f;
+      s->rem -= (double)s->nact * (fmin - s->v);
       s->v = fmin;
       s->t_last = te;
       int64_t m = 0;
@@ -587,6 +603,7 @@ static int b_run_to(bsim* b, double T) {
       }
       for (int64_t i = m; i < s->nact; ++i) s->act[i - m] = s->act[i];
       s->nact -= m;
+      if (s->nact == 0) s->rem = 0.0;
     } else {
       /* a KV lands: its request joins the decode batch */
       binst* s = &b->dec[k - P];
@@ -595,7 +612,7 @@ static int b_run_to(bsim* b, double T) {
       s->nwait--;
       b_advance(s, b->pt->beta_dec, te);
       s->owed_wait -= work_dec(b, r);
-      if (batch_insert(s, s->v + (double)work_dec(b, r), r)) return -2;
+      if (b_join(s, (double)work_dec(b, r), r)) return -2;
     }
   }
   if (T < INFINITY) {
@@ -606,10 +623,10 @@ static int b_run_to(bsim* b, double T) {
 }
 
 /* Features of one pool.  Clock backlog: the stand-alone work (ns) the
- * instance still owes, the batch's remaining virtual work summed in batch
- * order plus, on a decode instance, the whole work of the requests routed
- * there that have not joined (an exact integer), in seconds.  Ledger
- * backlog: as in the serial model. */
+ * instance still owes, the batch's running remaining work (clamped at 0)
+ * plus, on a decode instance, the whole work of the requests routed there
+ * that have not joined (an exact integer), in seconds.  Ledger backlog: as
+ * in the serial model. */
 static void batched_features(const bsim* b, int32_t pool, float* backlog, int64_t* queue, int64_t* kv) {
   const orc_point* pt = b->pt;
   const int32_t n = pool == ORC_PREFILL ? pt->n_prefill : pt->n_decode;
@@ -618,11 +635,7 @@ static void batched_features(const bsim* b, int32_t pool, float* backlog, int64_
     queue[j] = s->queue;
     kv[j] = s->kv;
     if (pt->backlog_mode == ORC_BACKLOG_TRUE) {
-      double w = 0.0;
-      for (int64_t i = 0; i < s->nact; ++i) {
-        const double rem = s->act[i].f - s->v;
-        w += rem < 0.0 ? 0.0 : rem; /* clamped as in b_next */
-      }
+      double w = s->rem < 0.0 ? 0.0 : s->rem;
       w += (double)s->owed_wait;
       backlog[j] = (float)w * 1e-9f;
     } else {
@@ -728,7 +741,7 @@ int orc_sim_replica_batched(const orc_point* pt, int64_t n, const int64_t* arriv
      * instance holds its cache and counts it from now, and takes it into its
      * batch when its KV lands */
     binst* a = &b.pre[ip];
-    if (batch_insert(a, a->v + (double)work_pre(&b, r), r)) {
+    if (b_join(a, (double)work_pre(&b, r), r)) {
       rc = -2;
       goto done;
     }

@@ -134,7 +134,7 @@ int point_mode(const rt_point& p) {
 bool class_fits(const rt::SimClass& c, const rt_point& p) {
   // the batched service model has one class of its own
   if ((c.kind == rt::kBat) != (p.service == RT_SERVICE_BATCHED)) return false;
-  if (c.kind == rt::kBat) return true;
+  if (c.kind == rt::kBat) return c.MP == 0 || p.n_prefill + p.n_decode <= c.S;
   if (c.kind == rt::kSeg) {
     if (c.mode != point_mode(p)) return false;
     const int lanes = (p.n_prefill + c.MP - 1) / c.MP + (p.n_decode + c.MD - 1) / c.MD;
@@ -376,11 +376,11 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   // Scratch of the serial classes: the dummy records, then the successor
   // records (kRecStride bytes each).
   bool any_serial = false;
-  int bat_class = -1;
+  std::vector<int> bat_classes;
   for (int c = 0; c < ncls; ++c) {
     if (buckets[c].empty()) continue;
     if (rt::sim_class(c).kind == rt::kBat)
-      bat_class = c;
+      bat_classes.push_back(c);
     else
       any_serial = true;
   }
@@ -396,19 +396,29 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
     if ((e = hipMalloc(&sim->d_scratch, need)) != hipSuccess) return hip_fail(e, "hipMalloc(scratch)");
     sim->scratch_bytes = need;
   }
-  // Scratch of the batched class: per-instance state and two rings per
-  // instance for every lane, sized by the largest pool and capacity among its
-  // replicas' points.
-  rt::BatScratch bs{};
-  if (bat_class >= 0) {
-    int32_t NI = 1, C = 2;
-    for (int32_t r : buckets[bat_class]) {
-      const rt_point& q = sim->points[pp[r]];
-      NI = std::max(NI, q.n_prefill + q.n_decode);
-      C = std::max(C, q.batch_cap == 0 ? kDefaultBatchCap : q.batch_cap);
+  // Scratch of the batched classes: per-instance state and two rings per
+  // instance for every lane of each, sized by the largest pool and capacity
+  // among that class's replicas' points; one allocation, carved in turn.
+  std::vector<rt::BatScratch> bs(ncls);
+  if (!bat_classes.empty()) {
+    struct Dim {
+      int64_t S;
+      int32_t NI, C;
+    };
+    std::vector<Dim> dims;
+    size_t bneed = 256;
+    for (int c : bat_classes) {
+      int32_t NI = 1, C = 2;
+      for (int32_t r : buckets[c]) {
+        const rt_point& q = sim->points[pp[r]];
+        NI = std::max(NI, q.n_prefill + q.n_decode);
+        C = std::max(C, q.batch_cap == 0 ? kDefaultBatchCap : q.batch_cap);
+      }
+      const rt::SimClass sc = rt::sim_class(c);
+      if (sc.MP == 1) NI = 1;  // a segment class: one instance per lane
+      dims.push_back(Dim{rt::bat_lanes(sc, (int64_t)buckets[c].size()), NI, C});
+      bneed += rt::bat_scratch_bytes(dims.back().S, NI, C);
     }
-    const int64_t S = (int64_t)buckets[bat_class].size();
-    const size_t bneed = rt::bat_scratch_bytes(S, NI, C) + 256;
     if (bneed > sim->bscratch_bytes) {
       if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
       if (sim->d_bscratch) (void)hipFree(sim->d_bscratch);
@@ -417,7 +427,11 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
       if ((e = hipMalloc(&sim->d_bscratch, bneed)) != hipSuccess) return hip_fail(e, "hipMalloc(batched scratch)");
       sim->bscratch_bytes = bneed;
     }
-    bs = rt::bat_scratch_carve(sim->d_bscratch, S, NI, C);
+    size_t at = 0;
+    for (size_t k = 0; k < bat_classes.size(); ++k) {
+      bs[bat_classes[k]] = rt::bat_scratch_carve(sim->d_bscratch + at, dims[k].S, dims[k].NI, dims[k].C);
+      at += rt::bat_scratch_bytes(dims[k].S, dims[k].NI, dims[k].C);
+    }
   }
   if ((size_t)n > sim->work_cap) {
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
@@ -507,7 +521,8 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
       where = sim->lanes[k];
       if ((e = hipStreamWaitEvent(where, sim->fork, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
-    e = rt::sim_class(c).kind == rt::kBat ? rt::launch_bat(a, bs, where) : rt::launch_sim(rt::sim_class(c), a, where);
+    e = rt::sim_class(c).kind == rt::kBat ? rt::launch_bat(rt::sim_class(c), a, bs[c], where)
+                                          : rt::launch_sim(rt::sim_class(c), a, where);
     if (e != hipSuccess) return hip_fail(e, "launch(sim)");
     if (act.size() > 1 && (e = hipEventRecord(sim->joins[k], where)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   }

@@ -79,12 +79,13 @@ struct Lane {
   __device__ double work_dec(int32_t o) const { return (double)(o - 1) * (double)pt.dec_tok_ns; }
 
   // Insert (key, r) into a ring of n entries starting at head, keeping
-  // (key, r) order: entries after it move one place back.
+  // (key, r) order: entries after it move one place back.  Returns the
+  // position taken, or -1 (and `full`) when the ring has no room.
   template <bool kBatch>
-  __device__ bool insert(int32_t j, int32_t head, int32_t n, double key, int32_t r) {
+  __device__ int32_t insert(int32_t j, int32_t head, int32_t n, double key, int32_t r) {
     if (n >= C) {
       full = true;
-      return false;
+      return -1;
     }
     int32_t i = head + n;
     while (i > head) {
@@ -96,7 +97,7 @@ struct Lane {
     Entry& d = kBatch ? member(j, i) : transfer(j, i);
     d.t = key;
     d.r = r;
-    return true;
+    return i;
   }
 
   // A prefill completion of request r at time tc: the instance lets go of
@@ -115,7 +116,7 @@ struct Lane {
     tmax = fmax(tmax, land);
     const int64_t k = at(d);
     const int32_t n = b.nw[k];
-    if (insert<false>(d, b.whead[k], n, land, r)) b.nw[k] = n + 1;
+    if (insert<false>(d, b.whead[k], n, land, r) >= 0) b.nw[k] = n + 1;
   }
 
   __device__ void decode_done(int32_t r, double tc, int32_t& q, double& kv, double& pend) {
@@ -136,7 +137,7 @@ struct Lane {
       if (now < kInf) b.tl[k] = now;
       return;
     }
-    double v = b.v[k], tl = b.tl[k], kv = b.kv[k], pend = b.pend[k];
+    double v = b.v[k], tl = b.tl[k], kv = b.kv[k], pend = b.pend[k], left = b.left[k];
     int32_t head = b.head[k], q = b.q[k];
     const double beta = pt.beta_pre;
     while (nact > 0 && !full) {
@@ -145,6 +146,7 @@ struct Lane {
       rem = rem < 0.0 ? 0.0 : rem;
       const double tc = tl + rem * slowdown(beta, nact);
       if (tc > now) break;
+      left = left - (double)nact * (e.t - v);
       v = e.t;
       tl = tc;
       tmax = fmax(tmax, tc);
@@ -156,12 +158,18 @@ struct Lane {
         e = member(j, head);
         if (e.t != v) break;
       }
+      if (nact == 0) left = 0.0;
     }
     if (now < kInf) {
-      if (nact > 0) v += (now - tl) / slowdown(beta, nact);
+      if (nact > 0) {
+        const double dv = (now - tl) / slowdown(beta, nact);
+        v = v + dv;
+        left = left - (double)nact * dv;
+      }
       tl = now;
     }
     b.v[k] = v;
+    b.left[k] = left;
     b.tl[k] = tl;
     b.kv[k] = kv;
     b.pend[k] = pend;
@@ -180,7 +188,7 @@ struct Lane {
       if (now < kInf) b.tl[k] = now;
       return;
     }
-    double v = b.v[k], tl = b.tl[k], kv = b.kv[k], pend = b.pend[k], owed = b.owed[k];
+    double v = b.v[k], tl = b.tl[k], kv = b.kv[k], pend = b.pend[k], owed = b.owed[k], left = b.left[k];
     int32_t head = b.head[k], q = b.q[k], wh = b.whead[k];
     const double beta = pt.beta_dec;
     while (!full) {
@@ -196,6 +204,7 @@ struct Lane {
       if (nact == 0 && nw == 0) break;
       if (tc <= tj) {
         if (tc > now) break;
+        left = left - (double)nact * (e.t - v);
         v = e.t;
         tl = tc;
         tmax = fmax(tmax, tc);
@@ -207,23 +216,36 @@ struct Lane {
           e = member(j, head);
           if (e.t != v) break;
         }
+        if (nact == 0) left = 0.0;
       } else {
         if (tj > now) break;
         const int32_t r = transfer(j, wh).r;
         ++wh;
         --nw;
-        if (nact > 0) v += (tj - tl) / slowdown(beta, nact);
+        if (nact > 0) {
+          const double dv = (tj - tl) / slowdown(beta, nact);
+          v = v + dv;
+          left = left - (double)nact * dv;
+        }
         tl = tj;
         const double w = work_dec(a.olen[lo + r]);
         owed = owed - w;
-        if (insert<true>(j, head, nact, v + w, r)) ++nact;
+        if (insert<true>(j, head, nact, v + w, r) >= 0) {
+          ++nact;
+          left = left + w;
+        }
       }
     }
     if (now < kInf) {
-      if (nact > 0) v += (now - tl) / slowdown(beta, nact);
+      if (nact > 0) {
+        const double dv = (now - tl) / slowdown(beta, nact);
+        v = v + dv;
+        left = left - (double)nact * dv;
+      }
       tl = now;
     }
     b.v[k] = v;
+    b.left[k] = left;
     b.tl[k] = tl;
     b.kv[k] = kv;
     b.pend[k] = pend;
@@ -240,18 +262,13 @@ struct Lane {
     for (int32_t d = 0; d < D && !full; ++d) run_decode(d, now);
   }
 
-  // Clock backlog of instance j in seconds: the batch's remaining virtual
-  // work in member order, then the owed work of requests not yet joined.
+  // Clock backlog of instance j in seconds: the batch's running remaining
+  // work (clamped at 0), then the owed work of requests not yet joined.
   __device__ float owed_s(int32_t j) {
     const int64_t k = at(j);
-    const int32_t nact = b.nact[k], head = b.head[k];
-    const double v = b.v[k];
-    double w = 0.0;
-    for (int32_t i = 0; i < nact; ++i) {
-      const double rem = member(j, head + i).t - v;
-      w += rem < 0.0 ? 0.0 : rem;
-    }
-    w += b.owed[k];
+    const double left = b.left[k];
+    double w = left < 0.0 ? 0.0 : left;
+    w = w + b.owed[k];
     return (float)w * 1e-9f;
   }
 
@@ -337,7 +354,7 @@ __global__ __launch_bounds__(kBlock) void bat_kernel(SimArgs a, BatScratch b) {
   L.wring = reinterpret_cast<Entry*>(b.wring) + lane * b.NI * (int64_t)b.C;
   for (int32_t j = 0; j < L.P + L.D; ++j) {
     const int64_t k = L.at(j);
-    b.v[k] = b.tl[k] = b.kv[k] = b.pend[k] = b.owed[k] = 0.0;
+    b.v[k] = b.tl[k] = b.kv[k] = b.pend[k] = b.owed[k] = b.left[k] = 0.0;
     b.q[k] = b.nact[k] = b.head[k] = b.nw[k] = b.whead[k] = 0;
   }
   bool rej = false;
@@ -379,8 +396,10 @@ __global__ __launch_bounds__(kBlock) void bat_kernel(SimArgs a, BatScratch b) {
     {
       const int64_t k = L.at(ip);
       const int32_t n = b.nact[k];
-      if (!L.insert<true>(ip, b.head[k], n, b.v[k] + L.work_pre(p), rl)) break;
+      const double w = L.work_pre(p);
+      if (L.insert<true>(ip, b.head[k], n, b.v[k] + w, rl) < 0) break;
       b.nact[k] = n + 1;
+      b.left[k] = b.left[k] + w;
       b.q[k] += 1;
       b.kv[k] = b.kv[k] + (double)p;
       b.pend[k] = b.pend[k] + (double)p;
@@ -399,6 +418,388 @@ __global__ __launch_bounds__(kBlock) void bat_kernel(SimArgs a, BatScratch b) {
   if (flag) atomicOr(a.flag, flag);
 }
 
+
+// ---------------------------------------------------------------------------
+// Segment variant: one replica per aligned segment of S lanes of a wave, one
+// instance per lane (prefill instances on lanes [0, P), decode instances on
+// [P, P + D)), as in the serial segment kernels.  A lane's instance state and
+// the front entries of its rings (with the front request's data) live in its
+// registers; the rings behind the fronts are the lane's own scratch.  Every
+// step (one request of every segment's replica) runs wave-uniform rounds:
+// prefill rounds, in each of which every prefill lane whose front completes
+// by the arrival lets it go and the decode lanes of the segment take the
+// departing KV transfers from it (read with cross-lane shuffles); decode
+// rounds, in each of which every decode lane takes its next event (a
+// completion, or a KV landing joining its batch); then every instance's clock
+// is brought to the arrival, every lane scores its instance, the two argmins
+// are DPP reductions over the segment, and the chosen lanes admit.  A round
+// pops one member per lane: members with equal finish virtual times leave in
+// consecutive rounds at the same time, with the same arithmetic as leaving
+// together (the remaining work they see is 0).
+struct RingTail {
+  double t;
+  int32_t r;
+};
+
+// Insert (key, r) into a ring of n entries from head: appended when it
+// follows the cached tail, else entries after it move back one place.
+// Returns the position taken, or -1 (and `full`) when the ring has no room.
+__device__ __forceinline__ int32_t ring_put(Entry* rg, int32_t C, int32_t head, int32_t n, double key, int32_t r,
+                                            RingTail& tail, bool& full) {
+  if (n >= C) {
+    full = true;
+    return -1;
+  }
+  int32_t i = head + n;
+  if (n == 0 || tail.t < key || (tail.t == key && tail.r < r)) {
+    Entry& d = rg[i & (C - 1)];
+    d.t = key;
+    d.r = r;
+    tail.t = key;
+    tail.r = r;
+    return i;
+  }
+  while (i > head) {
+    const Entry e = rg[(i - 1) & (C - 1)];
+    if (!(e.t > key || (e.t == key && e.r > r))) break;
+    rg[i & (C - 1)] = e;
+    --i;
+  }
+  Entry& d = rg[i & (C - 1)];
+  d.t = key;
+  d.r = r;
+  return i;
+}
+
+template <int S>
+__global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
+  const int lane = (int)(threadIdx.x & 63);
+  const int64_t gl = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  const int sl = lane & (S - 1);
+  const int base = lane & ~(S - 1);
+  const int64_t seg = gl / S;
+  const bool has = seg < a.n_work;
+  const int32_t rep = has ? a.work[seg] : 0;
+  const int64_t lo = has ? a.offsets[rep] : 0;
+  const int64_t len = has ? a.offsets[rep + 1] - lo : 0;
+  const DevPoint& pt = a.points[(has && a.param_point) ? a.param_point[rep] : 0];
+  const int32_t P = pt.P, D = pt.D;
+  const bool isP = has && sl < P;
+  const bool isD = has && sl >= P && sl < P + D;
+  const int32_t dme = sl - P;
+  const double beta = isP ? pt.beta_pre : pt.beta_dec;
+  const double xfer = (double)pt.xfer_tok_ns;
+  const int32_t C = b.C;
+  Entry* const ring = reinterpret_cast<Entry*>(b.ring) + gl * (int64_t)C;
+  Entry* const wring = reinterpret_cast<Entry*>(b.wring) + gl * (int64_t)C;
+
+  // instance state
+  double v = 0.0, tl = 0.0, left = 0.0, kv = 0.0, pend = 0.0, owed = 0.0;
+  int32_t q = 0, nact = 0, head = 0, nw = 0, wh = 0;
+  // batch front: finish virtual time, request, and its data (prefill:
+  // arrival, p, o, o^, decode instance; decode: prefill end, p, o, o^)
+  double f0 = 0.0, x0 = 0.0;
+  int32_t r0 = 0, p0 = 0, o0 = 0, oh0 = 0, dst0 = 0;
+  // transfer front (decode): landing time, request, its prefill end and data
+  double t0 = 0.0, pf1 = 0.0;
+  int32_t w0 = 0, p1 = 0, o1 = 0, oh1 = 0;
+  RingTail btail{0.0, 0}, wtail{0.0, 0};
+  double tmax = 0.0;
+  bool rej = false, full = false, dead = false;
+  int64_t last = -1;
+
+  // The front's data after a pop: the ring entry, then the request's data.
+  auto load_front = [&]() {
+    const Entry e = ring[head & (C - 1)];
+    f0 = e.t;
+    r0 = e.r;
+    const int64_t g = lo + e.r;
+    p0 = a.plen[g];
+    o0 = a.olen[g];
+    oh0 = a.ohat[g];
+    if (isP) {
+      x0 = i64_to_f64(a.arrival[g]);
+      dst0 = a.i_dec[g];
+    } else {
+      x0 = __longlong_as_double(a.span[g]);
+    }
+  };
+  auto load_transfer = [&]() {
+    const Entry e = wring[wh & (C - 1)];
+    t0 = e.t;
+    w0 = e.r;
+    const int64_t g = lo + e.r;
+    p1 = a.plen[g];
+    o1 = a.olen[g];
+    oh1 = a.ohat[g];
+    pf1 = __longlong_as_double(a.span[g]);
+  };
+
+  // Every event at or before `now` (prefill rounds, then decode rounds).
+  auto run_to = [&](double now) {
+    for (;;) {
+      double tc = kInf;
+      if (nact > 0) {
+        double rem = f0 - v;
+        rem = rem < 0.0 ? 0.0 : rem;
+        tc = tl + rem * slowdown(beta, nact);
+      }
+      const bool fire = isP && !dead && nact > 0 && tc <= now;
+      const uint64_t fm = __ballot(fire);
+      if (fm == 0) break;
+      double land = 0.0;
+      int32_t fr = 0, fd = 0, fp = 0, fo = 0, foh = 0;
+      if (fire) {
+        left = left - (double)nact * (f0 - v);
+        v = f0;
+        tl = tc;
+        tmax = fmax(tmax, tc);
+        const int64_t g = lo + r0;
+        q -= 1;
+        kv = kv - (double)p0;
+        pend = pend - (double)p0;
+        a.ttft[g] = round_ns(tc - x0);
+        a.span[g] = __double_as_longlong(tc);
+        land = tc + (double)p0 * xfer;
+        tmax = fmax(tmax, land);
+        fr = r0;
+        fd = dst0;
+        fp = p0;
+        fo = o0;
+        foh = oh0;
+        head += 1;
+        nact -= 1;
+        if (nact == 0)
+          left = 0.0;
+        else
+          load_front();
+      }
+      // the departing transfers go to their decode lanes: every position
+      // (within the segments) that fired somewhere in the wave is read by
+      // every lane from its own segment
+      uint64_t rel = 0;
+#pragma unroll
+      for (int s0 = 0; s0 < 64; s0 += S) rel |= (S == 64) ? fm : ((fm >> s0) & ((1ull << (S & 63)) - 1ull));
+      while (rel) {
+        const int i = __ffsll((unsigned long long)rel) - 1;
+        rel &= rel - 1;
+        const int src = base + i;
+        const bool fi = __shfl((int)fire, src) != 0;
+        const int32_t di = __shfl(fd, src);
+        const double li = __shfl(land, src);
+        const double ti = __shfl(tl, src);
+        const int32_t ri = __shfl(fr, src), pi = __shfl(fp, src), oi = __shfl(fo, src), ohi = __shfl(foh, src);
+        if (isD && fi && di == dme) {
+          const int32_t at = ring_put(wring, C, wh, nw, li, ri, wtail, full);
+          if (at >= 0) {
+            if (at == wh) {
+              t0 = li;
+              w0 = ri;
+              pf1 = ti;
+              p1 = pi;
+              o1 = oi;
+              oh1 = ohi;
+            }
+            nw += 1;
+          }
+        }
+      }
+    }
+    for (;;) {
+      double tc = kInf, tj = kInf;
+      if (nact > 0) {
+        double rem = f0 - v;
+        rem = rem < 0.0 ? 0.0 : rem;
+        tc = tl + rem * slowdown(beta, nact);
+      }
+      if (nw > 0) tj = t0;
+      const bool fire = isD && !dead && (nact > 0 || nw > 0) && (tc <= tj ? tc : tj) <= now;
+      if (!__any(fire)) break;
+      if (fire) {
+        if (tc <= tj) {
+          left = left - (double)nact * (f0 - v);
+          v = f0;
+          tl = tc;
+          tmax = fmax(tmax, tc);
+          const int64_t g = lo + r0;
+          q -= 1;
+          kv = kv - ((double)p0 + (double)o0);
+          pend = pend - (double)oh0;
+          a.span[g] = round_ns(tc - x0);
+          head += 1;
+          nact -= 1;
+          if (nact == 0)
+            left = 0.0;
+          else
+            load_front();
+        } else {
+          const int32_t r = w0, pr = p1, orr = o1, ohr = oh1;
+          const double pfr = pf1;
+          wh += 1;
+          nw -= 1;
+          if (nw > 0) load_transfer();
+          if (nact > 0) {
+            const double dv = (tj - tl) / slowdown(beta, nact);
+            v = v + dv;
+            left = left - (double)nact * dv;
+          }
+          tl = tj;
+          const double w = (double)(orr - 1) * (double)pt.dec_tok_ns;
+          owed = owed - w;
+          const double f = v + w;
+          const int32_t at = ring_put(ring, C, head, nact, f, r, btail, full);
+          if (at >= 0) {
+            if (at == head) {
+              f0 = f;
+              r0 = r;
+              x0 = pfr;
+              p0 = pr;
+              o0 = orr;
+              oh0 = ohr;
+            }
+            nact += 1;
+            left = left + w;
+          }
+        }
+      }
+    }
+  };
+
+  const int32_t Rmax = wave_max_nonneg((int32_t)len);
+  for (int32_t t = 0; t < Rmax; ++t) {
+    const bool mine = t < len && !dead;
+    const int64_t g = lo + t;
+    int64_t arr = 0;
+    int32_t p = 1, o = 1, oh = 1;
+    uint32_t c = 0;
+    uint4 ws = make_uint4(0u, 0u, 0u, 0u);
+    if (mine) {
+      arr = a.arrival[g];
+      p = a.plen[g];
+      o = a.olen[g];
+      oh = a.ohat[g];
+      c = a.cls[g];
+      if (pt.policy == kPolicyLearnedSampled) ws = *reinterpret_cast<const uint4*>(a.samp + 4 * g);
+    }
+    const bool valid = mine && p >= 1 && o >= 1 && oh >= 1 && (int64_t)p + o <= INT32_MAX &&
+                       (int64_t)p + oh <= INT32_MAX && (int32_t)c < pt.n_classes && arr >= 0 && arr >= last;
+    if (mine && !valid) {
+      rej = true;
+      if (sl == 0) {
+        a.i_pre[g] = a.i_dec[g] = -1;
+        a.ttft[g] = a.span[g] = -1;
+      }
+    }
+    const double now = valid ? i64_to_f64(arr) : -1.0;
+    if (valid) {
+      last = arr;
+      tmax = fmax(tmax, now);
+    }
+    run_to(now);
+    // The rounds end on every lane at once, but the compiler may represent
+    // their loops with per-lane exits and reuse a lane-mask compare made
+    // inside them (where it has no bits for lanes it considers gone) after
+    // them; passing the counts through opaque() makes every later test of
+    // them a fresh compare.
+    nact = opaque(nact);
+    nw = opaque(nw);
+    // every instance's clock to the arrival
+    if (valid && (isP || isD)) {
+      if (nact > 0) {
+        const double dv = (now - tl) / slowdown(beta, nact);
+        v = v + dv;
+        left = left - (double)nact * dv;
+      }
+      tl = now;
+    }
+    // each lane's key for its instance (0xffffffff: not offered)
+    uint32_t key = 0xffffffffu;
+    if (valid && (isP || isD)) {
+      const int32_t n = isP ? P : D;
+      const int32_t jj = isP ? sl : dme;
+      const int32_t pol = pt.policy;
+      if (pol == kPolicyRoundRobin) {
+        key = jj == t % n ? 0u : 1u;
+      } else if (pol == kPolicyLeastLoaded) {
+        key = (uint32_t)q;
+      } else if (pol == kPolicyLengthThreshold) {
+        const bool part = isP || n == 1 || ((jj >= (n + 1) / 2) == (oh >= pt.len_thr));
+        key = part ? (uint32_t)q : 0xffffffffu;
+      } else {
+        const float sg = pt.sigma[c];
+        const float work = isP ? pt.w_s * (float)p * pt.tau_pre : pt.w_s * (float)oh * pt.tau_dec;
+        const double need = isP ? (double)p : (double)p + (double)oh;
+        const float inv = isP ? pt.inv_cap_pre : pt.inv_cap_dec;
+        float bl;
+        if (pt.mode == 0) {
+          double w = left < 0.0 ? 0.0 : left;
+          w = w + owed;
+          bl = (float)w * 1e-9f;
+        } else if (isP) {
+          bl = pt.tau_pre * (float)pend + pt.pre_base * (float)q;
+        } else {
+          bl = pt.tau_dec * (float)pend;
+        }
+        const float press = (float)(kv + need) * inv;
+        const float load = pt.w_b * bl * sg;
+        const float size = work * (1.0f + pt.rho * press) * sg;
+        key = cost_key(load + size + pt.w_q * (float)q);
+        if (pol == kPolicyLearnedSampled) {
+          const uint32_t u = isP ? ws.x : ws.z, w2 = isP ? ws.y : ws.w;
+          const uint32_t c1 = __umulhi(u, (uint32_t)n);
+          const uint32_t x = __umulhi(w2, (uint32_t)(n - 1));
+          const uint32_t c2 = n > 1 ? x + (x >= c1 ? 1u : 0u) : c1;
+          key = ((uint32_t)jj == c1 || (uint32_t)jj == c2) ? key : 0xffffffffu;
+        }
+      }
+    }
+    uint32_t kp = isP ? key : 0xffffffffu, kd = isD ? key : 0xffffffffu;
+    const uint32_t kp0 = kp, kd0 = kd;
+    seg_min2<S>(kp, kd, lane);
+    const int32_t ip = seg_first<S>(isP && kp0 == kp, lane);
+    const int32_t id = seg_first<S>(isD && kd0 == kd, lane) - P;
+    if (valid) {
+      if (sl == 0) {
+        a.i_pre[g] = ip;
+        a.i_dec[g] = id;
+      }
+      if (isP && sl == ip) {
+        const double w = (double)pt.pre_base_ns + (double)p * (double)pt.pre_tok_ns;
+        const double f = v + w;
+        const int32_t at = ring_put(ring, C, head, nact, f, t, btail, full);
+        if (at >= 0) {
+          if (at == head) {
+            f0 = f;
+            r0 = t;
+            x0 = now;
+            p0 = p;
+            o0 = o;
+            oh0 = oh;
+            dst0 = id;
+          }
+          nact += 1;
+          q += 1;
+          kv = kv + (double)p;
+          pend = pend + (double)p;
+          left = left + w;
+        }
+      }
+      if (isD && dme == id) {
+        owed = owed + (double)(o - 1) * (double)pt.dec_tok_ns;
+        q += 1;
+        kv = kv + ((double)p + (double)o);
+        pend = pend + (double)oh;
+      }
+    }
+    // a replica whose ring overflowed stops (its outputs are not valid)
+    dead = seg_or<S>(full ? 1u : 0u, lane) != 0;
+  }
+  run_to(kInf);
+  const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u) |
+                        (full ? kFlagBatchCap : 0u);
+  if (flag) atomicOr(a.flag, flag);
+}
+
 }  // namespace bat
 
 // One allocation, 256-byte aligned arrays: the ten state arrays, then the
@@ -408,7 +809,7 @@ static size_t carve(char* base, int64_t S, int32_t NI, int32_t C, BatScratch* ou
   auto align = [](size_t x) { return (x + 255) & ~(size_t)255; };
   size_t off = 0;
   BatScratch b{};
-  double** d[] = {&b.v, &b.tl, &b.kv, &b.pend, &b.owed};
+  double** d[] = {&b.v, &b.tl, &b.kv, &b.pend, &b.owed, &b.left};
   for (double** x : d) {
     *x = reinterpret_cast<double*>(base + off);
     off = align(off + state * sizeof(double));
@@ -437,11 +838,25 @@ BatScratch bat_scratch_carve(char* base, int64_t S, int32_t NI, int32_t C) {
   return b;
 }
 
-hipError_t launch_bat(const SimArgs& a, const BatScratch& b, hipStream_t stream) {
+hipError_t launch_bat(const SimClass& c, const SimArgs& a, const BatScratch& b, hipStream_t stream) {
   if (a.n_work <= 0) return hipSuccess;
-  const int64_t blocks = (a.n_work + bat::kBlock - 1) / bat::kBlock;
-  hipLaunchKernelGGL(bat::bat_kernel, dim3((unsigned)blocks), dim3(bat::kBlock), 0, stream, a, b);
+  const int64_t lanes = a.n_work * (int64_t)c.S;
+  const dim3 grid((unsigned)((lanes + bat::kBlock - 1) / bat::kBlock)), block(bat::kBlock);
+#define RT_BSEG_CASE(S_)                                                              \
+  if (c.MP == 1 && c.S == S_) {                                                       \
+    hipLaunchKernelGGL((bat::bseg_kernel<S_>), grid, block, 0, stream, a, b);         \
+    return hipGetLastError();                                                         \
+  }
+  RT_BSEG_FOR_EACH(RT_BSEG_CASE)
+#undef RT_BSEG_CASE
+  hipLaunchKernelGGL(bat::bat_kernel, grid, block, 0, stream, a, b);
   return hipGetLastError();
+}
+
+// Lanes a launch of class c over n_work replicas spans (the scratch owners).
+int64_t bat_lanes(const SimClass& c, int64_t n_work) {
+  const int64_t lanes = n_work * (int64_t)c.S;
+  return (lanes + bat::kBlock - 1) / bat::kBlock * bat::kBlock;
 }
 
 }  // namespace rt

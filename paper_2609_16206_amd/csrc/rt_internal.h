@@ -101,7 +101,7 @@ SimClass sim_class(int i);
 // (a wave reads 64 consecutive elements); the rings are per lane, contiguous,
 // 16 bytes an entry, entry [((lane * NI + j) * C + pos].
 struct BatScratch {
-  double *v, *tl, *kv, *pend, *owed;       // [NI][S]
+  double *v, *tl, *kv, *pend, *owed, *left;  // [NI][S]; left: the batch's remaining work
   int32_t *q, *nact, *head, *nw, *whead;   // [NI][S]
   char* ring;   // batch members {f, request}, sorted by (f, request) from head
   char* wring;  // KV transfers in flight {landing time, request}, sorted likewise
@@ -113,7 +113,13 @@ struct BatScratch {
 // carving of one allocation into it.
 size_t bat_scratch_bytes(int64_t S, int32_t NI, int32_t C);
 BatScratch bat_scratch_carve(char* base, int64_t S, int32_t NI, int32_t C);
-hipError_t launch_bat(const SimArgs& a, const BatScratch& b, hipStream_t stream);
+// Batched classes: one replica per aligned segment of S lanes, one instance
+// per lane (P + D <= S; MP = MD = 1), then the general one, one replica per
+// lane (S = 1, MP = MD = 0).  bat_lanes: the lanes a launch spans, each the
+// owner of one state slot and one ring pair in the class's scratch.
+#define RT_BSEG_FOR_EACH(X) X(4) X(8) X(16) X(32) X(64)
+hipError_t launch_bat(const SimClass& c, const SimArgs& a, const BatScratch& b, hipStream_t stream);
+int64_t bat_lanes(const SimClass& c, int64_t n_work);
 
 struct ScoreArgs {
   float w_b, w_s, w_q, rho, tau, inv_cap;

@@ -25,14 +25,25 @@ constexpr int kNumWide = (int)(sizeof(kWideShapes) / sizeof(kWideShapes[0]));
 constexpr int kModes[] = {kModeTrue, kModeProxy, kModeBase, kModeTrueSampled, kModeProxySampled};
 constexpr int kNumModes = (int)(sizeof(kModes) / sizeof(kModes[0]));
 
+// Batched-service shapes {S, M}: the segment ones (M = 1), then the general
+// one-replica-per-lane class {1, 0}.
+#define RT_BSEG_SHAPE(S_) {S_, 1},
+const SegShape kBatShapes[] = {RT_BSEG_FOR_EACH(RT_BSEG_SHAPE){1, 0}};
+#undef RT_BSEG_SHAPE
+constexpr int kNumBat = (int)(sizeof(kBatShapes) / sizeof(kBatShapes[0]));
+
 }  // namespace
 
 // The one-wave and multi-wave classes of every mode, then the batched
-// service model's class (one replica per lane; its launch is launch_bat).
-int sim_class_count() { return (kNumShapes + kNumWide) * kNumModes + 1; }
+// service model's classes (one replica per lane; their launch is
+// launch_bat).
+int sim_class_count() { return (kNumShapes + kNumWide) * kNumModes + kNumBat; }
 
 SimClass sim_class(int i) {
-  if (i == (kNumShapes + kNumWide) * kNumModes) return SimClass{kBat, 1, 1, 1, kModeTrue};
+  if (i >= (kNumShapes + kNumWide) * kNumModes) {
+    const SegShape& e = kBatShapes[i - (kNumShapes + kNumWide) * kNumModes];
+    return SimClass{kBat, e.S, e.M, e.M, kModeTrue};
+  }
   if (i < kNumShapes * kNumModes) {
     const SegShape& e = kShapes[i % kNumShapes];
     return SimClass{kSeg, e.S, e.M, e.M, kModes[i / kNumShapes]};
