@@ -67,7 +67,8 @@ def _source_hash(files):
 
 SIM_SOURCES = ["paper_2609_16206_amd/csrc/" + f for f in (
     "seg_kernel.h", "wseg_kernel.h", "seg_true.hip", "seg_proxy.hip", "seg_base.hip", "seg_true_s.hip", "seg_proxy_s.hip", "seg_classes.hip",
-    "lane_ops.h", "rt_internal.h", "bat_kernel.hip")]
+    "lane_ops.h", "rt_internal.h")]
+BAT_SOURCES = ["paper_2609_16206_amd/csrc/" + f for f in ("bat_kernel.hip", "lane_ops.h", "rt_internal.h")]
 SCORE_SOURCES = ["paper_2609_16206_amd/csrc/score_kernel.hip", "paper_2609_16206_amd/csrc/rt_internal.h"]
 
 
@@ -164,8 +165,9 @@ def bench_sim(args):
     else:
         roof = dict(bound="alu", achieved=alg_ops / kernel_s / 1e12, peak=ALU_PEAK / 1e12, unit="Tlane-op/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = _traffic("sim", args.workload, SIM_SOURCES)
     batched = any(p.get("service") == "batched" for p in wl.points)
+    roof["traffic"] = _traffic("bat", args.workload, BAT_SOURCES) if batched else _traffic("sim", args.workload,
+                                                                                          SIM_SOURCES)
     roof["kernel"] = ("rt::bat::bseg_kernel / bat_kernel (the batched classes the call launches)" if batched else
                       "rt::seg::seg_kernel / wseg_kernel (every class one rt_sim_run_replicas call launches)")
     roof["kernel_ms"] = kernel_s * 1e3

@@ -471,6 +471,43 @@ __device__ __forceinline__ int32_t ring_put(Entry* rg, int32_t C, int32_t head, 
   return i;
 }
 
+// The first two entries of a ring, kept in registers: the front (valid when
+// the ring holds one entry or more) and the one behind it (two or more), so
+// that a departure needs no load before the next event time is known.
+struct Window {
+  double k0, k1;
+  int32_t r0, r1;
+};
+
+// After inserting (key, r) at position `at` of a ring whose head is `head`.
+__device__ __forceinline__ void window_put(Window& w, int32_t at, int32_t head, double key, int32_t r) {
+  const bool front = at == head, second = at == head + 1;
+  w.k1 = front ? w.k0 : (second ? key : w.k1);
+  w.r1 = front ? w.r0 : (second ? r : w.r1);
+  w.k0 = front ? key : w.k0;
+  w.r0 = front ? r : w.r0;
+}
+
+// After the front left a ring (head already advanced, n entries left): the
+// second becomes the front and the new second is loaded.
+__device__ __forceinline__ void window_pop(Window& w, const Entry* rg, int32_t C, int32_t head, int32_t n) {
+  w.k0 = w.k1;
+  w.r0 = w.r1;
+  if (n > 1) {
+    const Entry e = rg[(head + 1) & (C - 1)];
+    w.k1 = e.t;
+    w.r1 = e.r;
+  }
+}
+
+// One request's data, loaded a step ahead.
+struct Req {
+  int64_t arr;
+  int32_t p, o, oh;
+  uint32_t c;
+  uint4 ws;
+};
+
 template <int S>
 __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
   const int lane = (int)(threadIdx.x & 63);
@@ -489,6 +526,7 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
   const int32_t dme = sl - P;
   const double beta = isP ? pt.beta_pre : pt.beta_dec;
   const double xfer = (double)pt.xfer_tok_ns;
+  const bool samp = pt.policy == kPolicyLearnedSampled;
   const int32_t C = b.C;
   Entry* const ring = reinterpret_cast<Entry*>(b.ring) + gl * (int64_t)C;
   Entry* const wring = reinterpret_cast<Entry*>(b.wring) + gl * (int64_t)C;
@@ -496,24 +534,23 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
   // instance state
   double v = 0.0, tl = 0.0, left = 0.0, kv = 0.0, pend = 0.0, owed = 0.0;
   int32_t q = 0, nact = 0, head = 0, nw = 0, wh = 0;
-  // batch front: finish virtual time, request, and its data (prefill:
-  // arrival, p, o, o^, decode instance; decode: prefill end, p, o, o^)
-  double f0 = 0.0, x0 = 0.0;
-  int32_t r0 = 0, p0 = 0, o0 = 0, oh0 = 0, dst0 = 0;
-  // transfer front (decode): landing time, request, its prefill end and data
-  double t0 = 0.0, pf1 = 0.0;
-  int32_t w0 = 0, p1 = 0, o1 = 0, oh1 = 0;
+  // the batch's window and its front request's data (prefill: arrival, p,
+  // o, o^, decode instance; decode: prefill end, p, o, o^)
+  Window bw{0.0, 0.0, 0, 0};
+  double x0 = 0.0;
+  int32_t p0 = 0, o0 = 0, oh0 = 0, dst0 = 0;
+  // the transfers' window (decode) and the front transfer's data
+  Window tw{0.0, 0.0, 0, 0};
+  double pf1 = 0.0;
+  int32_t p1 = 0, o1 = 0, oh1 = 0;
   RingTail btail{0.0, 0}, wtail{0.0, 0};
   double tmax = 0.0;
   bool rej = false, full = false, dead = false;
   int64_t last = -1;
 
-  // The front's data after a pop: the ring entry, then the request's data.
-  auto load_front = [&]() {
-    const Entry e = ring[head & (C - 1)];
-    f0 = e.t;
-    r0 = e.r;
-    const int64_t g = lo + e.r;
+  // The data of the batch's new front (needed only when it leaves).
+  auto front_data = [&]() {
+    const int64_t g = lo + bw.r0;
     p0 = a.plen[g];
     o0 = a.olen[g];
     oh0 = a.ohat[g];
@@ -524,11 +561,8 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
       x0 = __longlong_as_double(a.span[g]);
     }
   };
-  auto load_transfer = [&]() {
-    const Entry e = wring[wh & (C - 1)];
-    t0 = e.t;
-    w0 = e.r;
-    const int64_t g = lo + e.r;
+  auto transfer_data = [&]() {
+    const int64_t g = lo + tw.r0;
     p1 = a.plen[g];
     o1 = a.olen[g];
     oh1 = a.ohat[g];
@@ -540,7 +574,7 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
     for (;;) {
       double tc = kInf;
       if (nact > 0) {
-        double rem = f0 - v;
+        double rem = bw.k0 - v;
         rem = rem < 0.0 ? 0.0 : rem;
         tc = tl + rem * slowdown(beta, nact);
       }
@@ -550,11 +584,11 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
       double land = 0.0;
       int32_t fr = 0, fd = 0, fp = 0, fo = 0, foh = 0;
       if (fire) {
-        left = left - (double)nact * (f0 - v);
-        v = f0;
+        left = left - (double)nact * (bw.k0 - v);
+        v = bw.k0;
         tl = tc;
         tmax = fmax(tmax, tc);
-        const int64_t g = lo + r0;
+        const int64_t g = lo + bw.r0;
         q -= 1;
         kv = kv - (double)p0;
         pend = pend - (double)p0;
@@ -562,17 +596,19 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
         a.span[g] = __double_as_longlong(tc);
         land = tc + (double)p0 * xfer;
         tmax = fmax(tmax, land);
-        fr = r0;
+        fr = bw.r0;
         fd = dst0;
         fp = p0;
         fo = o0;
         foh = oh0;
         head += 1;
         nact -= 1;
-        if (nact == 0)
+        if (nact == 0) {
           left = 0.0;
-        else
-          load_front();
+        } else {
+          window_pop(bw, ring, C, head, nact);
+          front_data();
+        }
       }
       // the departing transfers go to their decode lanes: every position
       // (within the segments) that fired somewhere in the wave is read by
@@ -592,9 +628,8 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
         if (isD && fi && di == dme) {
           const int32_t at = ring_put(wring, C, wh, nw, li, ri, wtail, full);
           if (at >= 0) {
+            window_put(tw, at, wh, li, ri);
             if (at == wh) {
-              t0 = li;
-              w0 = ri;
               pf1 = ti;
               p1 = pi;
               o1 = oi;
@@ -608,36 +643,41 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
     for (;;) {
       double tc = kInf, tj = kInf;
       if (nact > 0) {
-        double rem = f0 - v;
+        double rem = bw.k0 - v;
         rem = rem < 0.0 ? 0.0 : rem;
         tc = tl + rem * slowdown(beta, nact);
       }
-      if (nw > 0) tj = t0;
+      if (nw > 0) tj = tw.k0;
       const bool fire = isD && !dead && (nact > 0 || nw > 0) && (tc <= tj ? tc : tj) <= now;
       if (!__any(fire)) break;
       if (fire) {
         if (tc <= tj) {
-          left = left - (double)nact * (f0 - v);
-          v = f0;
+          left = left - (double)nact * (bw.k0 - v);
+          v = bw.k0;
           tl = tc;
           tmax = fmax(tmax, tc);
-          const int64_t g = lo + r0;
+          const int64_t g = lo + bw.r0;
           q -= 1;
           kv = kv - ((double)p0 + (double)o0);
           pend = pend - (double)oh0;
           a.span[g] = round_ns(tc - x0);
           head += 1;
           nact -= 1;
-          if (nact == 0)
+          if (nact == 0) {
             left = 0.0;
-          else
-            load_front();
+          } else {
+            window_pop(bw, ring, C, head, nact);
+            front_data();
+          }
         } else {
-          const int32_t r = w0, pr = p1, orr = o1, ohr = oh1;
+          const int32_t r = tw.r0, pr = p1, orr = o1, ohr = oh1;
           const double pfr = pf1;
           wh += 1;
           nw -= 1;
-          if (nw > 0) load_transfer();
+          if (nw > 0) {
+            window_pop(tw, wring, C, wh, nw);
+            transfer_data();
+          }
           if (nact > 0) {
             const double dv = (tj - tl) / slowdown(beta, nact);
             v = v + dv;
@@ -649,9 +689,8 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
           const double f = v + w;
           const int32_t at = ring_put(ring, C, head, nact, f, r, btail, full);
           if (at >= 0) {
+            window_put(bw, at, head, f, r);
             if (at == head) {
-              f0 = f;
-              r0 = r;
               x0 = pfr;
               p0 = pr;
               o0 = orr;
@@ -665,22 +704,32 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
     }
   };
 
+  auto fetch = [&](int32_t t) {
+    Req q0{0, 1, 1, 1, 0u, make_uint4(0u, 0u, 0u, 0u)};
+    if (t < len) {
+      const int64_t g = lo + t;
+      q0.arr = a.arrival[g];
+      q0.p = a.plen[g];
+      q0.o = a.olen[g];
+      q0.oh = a.ohat[g];
+      q0.c = a.cls[g];
+      if (samp) q0.ws = *reinterpret_cast<const uint4*>(a.samp + 4 * g);
+    }
+    return q0;
+  };
+
   const int32_t Rmax = wave_max_nonneg((int32_t)len);
+  Req nx = fetch(0);
   for (int32_t t = 0; t < Rmax; ++t) {
+    // request t, loaded a step ahead; request t + 1 is loaded now
+    const Req cur = nx;
+    nx = fetch(t + 1);
+    const int64_t arr = cur.arr;
+    const int32_t p = cur.p, o = cur.o, oh = cur.oh;
+    const uint32_t c = cur.c;
+    const uint4 ws = cur.ws;
     const bool mine = t < len && !dead;
     const int64_t g = lo + t;
-    int64_t arr = 0;
-    int32_t p = 1, o = 1, oh = 1;
-    uint32_t c = 0;
-    uint4 ws = make_uint4(0u, 0u, 0u, 0u);
-    if (mine) {
-      arr = a.arrival[g];
-      p = a.plen[g];
-      o = a.olen[g];
-      oh = a.ohat[g];
-      c = a.cls[g];
-      if (pt.policy == kPolicyLearnedSampled) ws = *reinterpret_cast<const uint4*>(a.samp + 4 * g);
-    }
     const bool valid = mine && p >= 1 && o >= 1 && oh >= 1 && (int64_t)p + o <= INT32_MAX &&
                        (int64_t)p + oh <= INT32_MAX && (int32_t)c < pt.n_classes && arr >= 0 && arr >= last;
     if (mine && !valid) {
@@ -768,9 +817,8 @@ __global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
         const double f = v + w;
         const int32_t at = ring_put(ring, C, head, nact, f, t, btail, full);
         if (at >= 0) {
+          window_put(bw, at, head, f, t);
           if (at == head) {
-            f0 = f;
-            r0 = t;
             x0 = now;
             p0 = p;
             o0 = o;
