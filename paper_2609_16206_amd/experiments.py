@@ -14,7 +14,11 @@ the router:
     of scales in one batch and refining inside the bracketing interval;
   * fit_service_constants: the calibration step (Section III-B): prices
     per prompt and per output token fitted to latency curves by least
-    squares.
+    squares;
+  * service_cells / the `service` study: the serial-service model next to
+    continuous batching in both stages (Section VI's correction), per
+    policy at one arrival rate, with goodput and tail TTFT, and the
+    saturation scale under each model.
 
 Replica streams: cell c's replica k draws from replica index
 c * stride + k of the workload seed, so cells never share draws.
@@ -55,9 +59,11 @@ def build_trace(cells: Sequence[Cell], replicas: int, requests: int, seed: int,
 
 
 def run_cells(cells: Sequence[Cell], replicas: int = 32, requests: int = 5000, seed: int = 0,
-              device: int = 0, return_trace: bool = False):
-    """Goodput per cell: a list of dicts (label, mean, std, min, max), and
-    optionally the trace and per-replica goodput."""
+              device: int = 0, return_trace: bool = False, ttft_tail: bool = False):
+    """Goodput per cell: a list of dicts (label, mean, std, min, max; with
+    `ttft_tail` also the median and 99th-percentile TTFT in seconds over
+    the cell's requests), and optionally the trace and per-replica
+    goodput."""
     import torch
 
     tr = build_trace(cells, replicas, requests, seed)
@@ -68,7 +74,7 @@ def run_cells(cells: Sequence[Cell], replicas: int = 32, requests: int = 5000, s
         g, _ = sim.goodput(dtr, out)
         flags = sim.data_status()
         g = g.cpu().numpy()
-        outs = {k: v.cpu().numpy() for k, v in out.items()} if return_trace else None
+        outs = {k: v.cpu().numpy() for k, v in out.items()} if (return_trace or ttft_tail) else None
         torch.cuda.synchronize(device)
     finally:
         sim.close()
@@ -77,8 +83,14 @@ def run_cells(cells: Sequence[Cell], replicas: int = 32, requests: int = 5000, s
     rows = []
     for c, cell in enumerate(cells):
         x = g[c * replicas:(c + 1) * replicas]
-        rows.append(dict(label=cell.label, mean=float(x.mean()), std=float(x.std()), min=float(x.min()),
-                         max=float(x.max())))
+        row = dict(label=cell.label, mean=float(x.mean()), std=float(x.std()), min=float(x.min()),
+                   max=float(x.max()))
+        if ttft_tail:
+            t = outs["ttft_ns"][c * replicas * requests:(c + 1) * replicas * requests]
+            t = t[t >= 0] * 1e-9
+            row["ttft_p50_s"] = float(np.percentile(t, 50)) if t.size else None
+            row["ttft_p99_s"] = float(np.percentile(t, 99)) if t.size else None
+        rows.append(row)
     if return_trace:
         return rows, tr, outs, g
     return rows
@@ -185,6 +197,24 @@ def noise_cells(P: int, D: int, traffic: W.Traffic, sigmas=(0.0, 0.3, 0.6, 0.9, 
     return [Cell(f"sigma {s:g}", pt, W.with_predictor_sigma(traffic, s)) for s in sigmas]
 
 
+# Room per instance for batch members and KV transfers in flight in the
+# service study: near saturation a batched instance holds hundreds.
+BATCH_ROOM = 4096
+
+
+def service_cells(P: int, D: int, traffic: W.Traffic, policies=("learned", "round_robin", "least_loaded"),
+                  beta: float = W.BATCH_BETA, **kw) -> List[Cell]:
+    """Each policy under the serial-service model and under continuous
+    batching in both stages (Section VI), at the same arrival rate."""
+    cells = []
+    for pol in policies:
+        for sv in ("serial", "batched"):
+            pt = W.make_point(P, D, n_classes=3, policy=pol, service=sv, beta_pre=beta, beta_dec=beta, **kw)
+            pt["batch_cap"] = BATCH_ROOM
+            cells.append(Cell(f"{pol} {sv}", pt, traffic))
+    return cells
+
+
 def width_cells(P: int, widths: Sequence[int], traffic: W.Traffic, policies=("learned", "round_robin"),
                 **kw) -> List[Cell]:
     """Decode-pool widths at a fixed arrival rate (Section V-D)."""
@@ -204,7 +234,8 @@ def main(argv=None) -> None:
     import json
 
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
-    ap.add_argument("study", choices=["saturation", "policies", "ablation", "noise", "width", "calibrate"])
+    ap.add_argument("study", choices=["saturation", "policies", "ablation", "noise", "width", "calibrate",
+                                      "service"])
     ap.add_argument("--traffic", default="mixed", choices=sorted(TRAFFIC))
     ap.add_argument("--prefill", type=int, default=2)
     ap.add_argument("--decode", type=int, default=4)
@@ -219,6 +250,20 @@ def main(argv=None) -> None:
     if a.study == "calibrate":
         fit = fit_service_constants(**latency_curves(pt, noise=0.05, seed=a.seed))
         print(json.dumps(fit))
+        return
+    if a.study == "service":
+        # round robin's saturation scale under each model, then every
+        # policy under both at the serial model's saturation scale
+        sat = {sv: saturation_scale(dict(pt, service=sv, beta_pre=W.BATCH_BETA, beta_dec=W.BATCH_BETA,
+                                         batch_cap=BATCH_ROOM), traf,
+                                    scales=tuple(np.geomspace(0.25, 1024.0, 13)), replicas=a.replicas,
+                                    requests=a.requests, seed=a.seed)["scale"]
+               for sv in ("serial", "batched")}
+        print(json.dumps(dict(saturation_scale=sat, note="None: no collapse within the probed scales 0.25-1024")))
+        scale = a.scale if a.scale is not None else sat["serial"]
+        for r in run_cells(service_cells(a.prefill, a.decode, traf.scaled(scale)), a.replicas, a.requests, a.seed,
+                           ttft_tail=True):
+            print(json.dumps(dict(r, scale=scale)))
         return
     scale = a.scale
     if scale is None or a.study == "saturation":

@@ -54,3 +54,18 @@ def test_noise_cells_change_only_the_prediction():
         assert np.array_equal(t0[k], t1[k]), k
     assert np.array_equal(t0["pred_out_len"], np.maximum(1, t0["out_len"]))
     assert not np.array_equal(t1["pred_out_len"], t0["pred_out_len"])
+
+
+def test_service_cells_pair_each_policy():
+    """The service study pairs every policy's serial cell with its batched
+    cell at the same traffic and betas (Section VI's correction)."""
+    traf = W.mixed_bursty()
+    cells = E.service_cells(2, 4, traf, policies=("learned", "round_robin"), beta=0.01)
+    assert [c.label for c in cells] == ["learned serial", "learned batched", "round_robin serial",
+                                        "round_robin batched"]
+    for a, b in zip(cells[0::2], cells[1::2]):
+        assert a.point["service"] == "serial" and b.point["service"] == "batched"
+        assert b.point["beta_pre"] == b.point["beta_dec"] == 0.01
+        assert a.traffic is b.traffic
+        assert {k: v for k, v in a.point.items() if k != "service"} == {k: v for k, v in b.point.items()
+                                                                       if k != "service"}
