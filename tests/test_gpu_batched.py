@@ -163,3 +163,18 @@ def test_determinism_and_range_resume():
     for k in a:
         assert np.array_equal(a[k][s], c[k]), k
     assert np.array_equal(ga[117:211], gc)
+
+
+def test_wide_bench_workload_sampled():
+    """The 65,536 x 2,000 batched bench workload in the launch configuration
+    bench.py times: properties on every request, goodput recount on every
+    replica, and follow-mode parity on a spread sample of replicas."""
+    wl = W.paper_cluster(n_replicas=65536, requests=2000, service="batched")
+    tr = W.make_trace(wl)
+    gpu, g, met, flags = run_sim(wl.points, tr)
+    assert flags == 0
+    check_properties(wl.points, tr, gpu)
+    assert np.array_equal(goodput_recount(wl.points, tr, gpu), met)
+    sample = list(range(0, 65536, 1021)) + [65535]
+    rep = follow_replicas(wl.points, tr, gpu, sample, gpu_goodput=g, gpu_met=met)
+    log(f"batched 65536x2000: {rep}; mean goodput {g.mean():.4f}")
