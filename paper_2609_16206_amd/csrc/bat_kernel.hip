@@ -15,25 +15,28 @@
 // completion lies at t_last + max(f_front - v, 0) (1 + beta (b - 1)).
 //
 // Mapping.  A replica is a chain of events with a data-dependent number of
-// events per arrival (completions, KV landings), and replicas are
-// independent: one replica per lane.  Between two arrivals the prefill
-// instances evolve alone (nothing but arrivals feeds them) and each decode
-// instance evolves from its own completions and the KV landings that the
-// prefill completions up to that arrival scheduled, so a lane processes each
-// prefill instance's events up to the arrival, then each decode instance's;
+// events per arrival (completions, KV landings); replicas are independent.
+// Between two arrivals the prefill instances evolve alone (nothing but
+// arrivals feeds them), and each decode instance evolves from its own
+// completions and the KV landings that the prefill completions up to that
+// arrival scheduled.  So every instance's events up to an arrival can be
+// taken prefill pool first, then decode pool, each instance in time order:
 // every instance sees the same sequence of events, in the same order and
-// with the same arithmetic, as a global time-ordered loop.  Per-instance
-// scalars are structure-of-arrays (the lanes of a wave read one contiguous
-// line per field); batch members and KV transfers in flight are sorted rings
-// of 16-byte entries, contiguous per lane, so the walk over a batch (the
-// backlog sum, an insertion) stays within a few cache lines.
+// with the same arithmetic, as a global time-ordered loop.  Two kernels do
+// this: bseg_kernel (below), one replica per segment of S <= 64 lanes and one
+// instance per lane, for points with P + D <= 64; and bat_kernel, one replica
+// per lane walking its instances in turn, for any point.  Batch members and
+// KV transfers in flight are sorted rings in scratch, contiguous per lane.
 //
 // Arithmetic.  Times are float64 ns; every operation matches the written
 // model one for one (built with -ffp-contract=off): s = 1 + beta * (b - 1),
-// v += (t - t_last) / s, tc = t_last + max(f - v, 0) * s.  Token totals and
-// the owed decode work of requests not yet joined are exact integers in
-// doubles.  The cost equation is the serial kernels' (float32, written
-// order).  Outputs round to whole ns, nearest with ties to even.
+// dv = (t - t_last) / s, v += dv, tc = t_last + max(f - v, 0) * s.  The
+// batch's remaining stand-alone work is a running total (+ the work of each
+// joining member, - b * dv at each clock step, - b * (f - v) when a member
+// leaves, 0 once the batch empties), read clamped at 0 as the clock backlog.
+// Token totals and the owed decode work of requests not yet joined are exact
+// integers in doubles.  The cost equation is the serial kernels' (float32,
+// written order).  Outputs round to whole ns, nearest with ties to even.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -58,7 +61,9 @@ __device__ __forceinline__ double slowdown(double beta, int32_t b) { return 1.0 
 // Nearest integer of a double in [0, 2^52), ties to even, as an int64.
 __device__ __forceinline__ int64_t round_ns(double x) { return f64_to_i64(__builtin_rint(x)); }
 
-// One lane's replica: its point, its request arrays and its scratch.
+// bat_kernel's lane: its replica's point, request arrays and scratch.  The
+// per-instance scalars are structure-of-arrays, element [j * S + lane] (the
+// lanes of a wave read one contiguous line per field); entries are 16 bytes.
 struct Lane {
   const SimArgs& a;
   const BatScratch& b;
