@@ -233,9 +233,12 @@ typedef struct {
  * The call reads offsets and param_point back to the host to plan the launch
  * (it synchronizes `hip_stream` for that), validates them (RT_EINVAL), then
  * enqueues the simulation on `hip_stream` and returns.  Scratch memory grows
- * with n_requests (80 bytes per request), and for batched replicas with
- * (P + D) x (64 + 32 batch_cap) bytes per replica (largest P + D and
- * batch_cap of the call's batched points); it is owned by `sim`. */
+ * with n_requests (80 bytes per request, for serial points), and for
+ * batched replicas with about 68 + 32 batch_cap bytes per instance slot: a
+ * replica of a point with P + D <= 64 takes S slots, S the smallest of 4, 8,
+ * 16, 32, 64 that holds P + D; a larger point takes P + D slots (each kind
+ * sized by the largest pool and batch_cap among the call's points of that
+ * kind).  It is owned by `sim`. */
 rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* out, void* hip_stream);
 
 /* Per-replica goodput: the fraction of the replica's requests that meet both
