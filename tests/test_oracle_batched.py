@@ -270,3 +270,31 @@ def test_bad_beta_rejected():
         pt = W.make_point(2, 2, n_classes=3, service="batched", beta_dec=bad)
         with pytest.raises(ValueError):
             O.sim_replica(pt, a, p, o, oh, c)
+
+
+def test_random_tiny_traces_match_exact_brute_force():
+    """Many random tiny traces on a coarse time grid (simultaneous arrivals,
+    equal works, so equal finish times and landings at equal times are
+    frequent), every policy, dyadic betas (so exact rationals stay small):
+    the oracle following the brute force's placements has no divergence
+    beyond a near-tie and its times are the exact ones rounded (within 1 ns
+    where the exact value is within 1e-4 ns of a half)."""
+    rng = np.random.default_rng(77)
+    pols = POLICIES
+    for trial in range(150):
+        P, D = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        n = int(rng.integers(1, 13))
+        policy, mode = pols[trial % len(pols)]
+        pt = W.make_point(P, D, n_classes=2, policy=policy, backlog_mode=mode, service="batched",
+                          beta_pre=float(rng.choice([0.0, 0.125, 0.5, 1.0])),
+                          beta_dec=float(rng.choice([0.0, 0.25, 1.0])), len_threshold=3)
+        pt.update(pre_base_ns=int(rng.choice([0, 4])), pre_tok_ns=int(rng.choice([1, 2])),
+                  dec_tok_ns=int(rng.choice([1, 3])), xfer_tok_ns=int(rng.choice([0, 1])))
+        a = np.sort(rng.integers(0, 8, n)).astype(np.int64) * 4
+        p = rng.integers(1, 5, n).astype(np.int32)
+        o = rng.integers(1, 5, n).astype(np.int32)
+        oh = rng.integers(1, 6, n).astype(np.int32)
+        c = rng.integers(0, 2, n).astype(np.uint8)
+        words = rng.integers(0, 2 ** 32, (n, 4), dtype=np.uint64).astype(np.uint32)
+        ref = simulate_batched(pt, a, p, o, oh, c, words=words, exact=True)
+        _follow_check(pt, a, p, o, oh, c, words, ref, exact=ref["exact"])
