@@ -72,7 +72,9 @@ def test_mixed_shapes_betas_and_serial_points():
     """Batched points of several pool shapes and betas (0: infinite server;
     1: pure processor sharing) next to serial points in one call, so both
     kernel kinds run side by side; ragged and empty replicas."""
-    shapes = [(1, 1), (2, 6), (3, 9), (5, 16), (8, 8), (33, 64), (2, 2), (4, 12)]
+    # segment widths 4, 8, 16, 32 and 64 (P + D = 64 exactly), and beyond 64
+    # instances the one-replica-per-lane kernel
+    shapes = [(1, 1), (2, 6), (3, 9), (5, 16), (8, 8), (33, 64), (2, 2), (4, 12), (32, 32), (20, 44)]
     betas = [(0.0, 0.0), (W.BATCH_BETA, W.BATCH_BETA), (1.0, 0.25), (0.5, 1.0)]
     pts = []
     for k, (P, D) in enumerate(shapes):
