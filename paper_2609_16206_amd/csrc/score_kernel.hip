@@ -175,16 +175,38 @@ __global__ void __launch_bounds__(kBlock) goodput_kernel(GoodputArgs a) {
     }
     return;
   }
+  // the point's targets, lane k < 8 holding class k's (read per request
+  // with a cross-lane shuffle instead of a dependent load)
   const DevPoint& pp = a.points[pid];
+  const int k8 = lane & (kMaxClasses - 1);
+  const int64_t my_ttft = pp.slo_ttft[k8], my_tpot = pp.slo_tpot[k8];
   int64_t met = 0;
-  for (int64_t i = lo + lane; i < hi; i += 64) {
-    const int64_t tt = a.ttft[i], sp = a.span[i];
-    const int32_t o = a.olen[i];
-    const uint32_t c = a.cls[i];
-    if (tt < 0 || c >= (uint32_t)kMaxClasses) continue;
-    const bool ok_ttft = tt <= pp.slo_ttft[c];
-    const bool ok_tpot = o <= 1 || sp <= pp.slo_tpot[c] * (int64_t)(o - 1);
-    met += (ok_ttft && ok_tpot) ? 1 : 0;
+  // four 64-request chunks per iteration, their loads issued together
+  constexpr int kU = 4;
+  for (int64_t i0 = lo; i0 < hi; i0 += 64 * kU) {
+    int64_t tt[kU], sp[kU];
+    int32_t o[kU];
+    uint32_t c[kU];
+    bool in[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int64_t i = i0 + u * 64 + lane;
+      in[u] = i < hi;
+      const int64_t j = in[u] ? i : lo;
+      tt[u] = a.ttft[j];
+      sp[u] = a.span[j];
+      o[u] = a.olen[j];
+      c[u] = a.cls[j];
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const bool valid = in[u] && tt[u] >= 0 && c[u] < (uint32_t)kMaxClasses;
+      const int cc = valid ? (int)c[u] : 0;
+      const int64_t lim_ttft = __shfl(my_ttft, cc, 64), lim_tpot = __shfl(my_tpot, cc, 64);
+      const bool ok_ttft = tt[u] <= lim_ttft;
+      const bool ok_tpot = o[u] <= 1 || sp[u] <= lim_tpot * (int64_t)(o[u] - 1);
+      met += (valid && ok_ttft && ok_tpot) ? 1 : 0;
+    }
   }
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) {
