@@ -513,8 +513,11 @@ struct Req {
   uint4 ws;
 };
 
-template <int S>
-__global__ __launch_bounds__(kBlock) void bseg_kernel(SimArgs a, BatScratch b) {
+// kMinBlocks: workgroups per compute unit the register budget must allow
+// (1: as many registers as the kernel wants, for launches whose waves do not
+// fill the GPU; 3: three waves per SIMD, for launches with many waves).
+template <int S, int kMinBlocks>
+__global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, BatScratch b) {
   const int lane = (int)(threadIdx.x & 63);
   const int64_t gl = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   const int sl = lane & (S - 1);
@@ -895,9 +898,15 @@ hipError_t launch_bat(const SimClass& c, const SimArgs& a, const BatScratch& b, 
   if (a.n_work <= 0) return hipSuccess;
   const int64_t lanes = a.n_work * (int64_t)c.S;
   const dim3 grid((unsigned)((lanes + bat::kBlock - 1) / bat::kBlock)), block(bat::kBlock);
+  // with at least two waves per SIMD to place, occupancy pays more than
+  // registers do
+  const bool many = lanes >= 2 * 64 * 1024;
 #define RT_BSEG_CASE(S_)                                                              \
   if (c.MP == 1 && c.S == S_) {                                                       \
-    hipLaunchKernelGGL((bat::bseg_kernel<S_>), grid, block, 0, stream, a, b);         \
+    if (many)                                                                         \
+      hipLaunchKernelGGL((bat::bseg_kernel<S_, 3>), grid, block, 0, stream, a, b);    \
+    else                                                                              \
+      hipLaunchKernelGGL((bat::bseg_kernel<S_, 1>), grid, block, 0, stream, a, b);    \
     return hipGetLastError();                                                         \
   }
   RT_BSEG_FOR_EACH(RT_BSEG_CASE)
