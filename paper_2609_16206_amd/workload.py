@@ -40,9 +40,9 @@ import numpy as np
 
 MAX_CLASSES = 8
 
-POLICIES = {"learned": 0, "round_robin": 1, "least_loaded": 2}
-BACKLOG_MODES = {"true": 0, "proxy": 1}
-POOLS = {"prefill": 0, "decode": 1}
+POLICIES = ("learned", "round_robin", "least_loaded", "learned_sampled", "length_threshold")
+BACKLOG_MODES = ("true", "proxy")
+SERVICES = ("serial", "batched")
 
 
 def f32(x: float) -> float:
@@ -138,8 +138,8 @@ def make_point(
     link_bytes_per_s: float = LINK_BYTES_PER_S,
     len_threshold: int = 256,
     service: str = "serial",
-    beta_pre: float = None,
-    beta_dec: float = None,
+    beta_pre: Optional[float] = None,
+    beta_dec: Optional[float] = None,
 ) -> Dict:
     """One parameter point: pool shape, router constants, physics and SLOs.
 
