@@ -180,3 +180,37 @@ def test_wide_bench_workload_sampled():
     sample = list(range(0, 65536, 1021)) + [65535]
     rep = follow_replicas(wl.points, tr, gpu, sample, gpu_goodput=g, gpu_met=met)
     log(f"batched 65536x2000: {rep}; mean goodput {g.mean():.4f}")
+
+
+def test_coarse_grid_ties_many_small_replicas():
+    """Hundreds of small replicas on a coarse time grid with tiny integer
+    physics and transfers of zero: simultaneous arrivals, equal finish times
+    within a batch, completions and KV landings at the same instant, zero
+    decode work (o = 1).  Every replica is checked against the oracle."""
+    rng = np.random.default_rng(91)
+    pts = []
+    for k in range(12):
+        pol, mode = POLICIES[k % len(POLICIES)]
+        pt = _batched(W.make_point(int(rng.integers(1, 4)), int(rng.integers(1, 4)), n_classes=2, policy=pol,
+                                   backlog_mode=mode, len_threshold=3),
+                      float(rng.choice([0.0, 0.125, 0.5, 1.0])), float(rng.choice([0.0, 0.25, 1.0])))
+        pt.update(pre_base_ns=int(rng.choice([0, 4])), pre_tok_ns=int(rng.choice([1, 2])),
+                  dec_tok_ns=int(rng.choice([1, 3])), xfer_tok_ns=int(rng.choice([0, 1])))
+        pts.append(pt)
+    n_rep = 480
+    lengths = rng.integers(1, 41, n_rep)
+    parts = {k: [] for k in ("arrival_ns", "prompt_len", "out_len", "pred_out_len", "slo_class")}
+    for n in lengths:
+        parts["arrival_ns"].append(np.sort(rng.integers(0, 12, n)).astype(np.int64) * 4)
+        parts["prompt_len"].append(rng.integers(1, 5, n).astype(np.int32))
+        parts["out_len"].append(rng.integers(1, 5, n).astype(np.int32))
+        parts["pred_out_len"].append(rng.integers(1, 6, n).astype(np.int32))
+        parts["slo_class"].append(rng.integers(0, 2, n).astype(np.uint8))
+    tr = {k: np.concatenate(v) for k, v in parts.items()}
+    tr["offsets"] = np.concatenate(([0], np.cumsum(lengths))).astype(np.int64)
+    tr["param_point"] = (np.arange(n_rep) % len(pts)).astype(np.int32)
+    W.add_sample_words(tr, 91)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    rep = follow_replicas(pts, tr, gpu, range(n_rep), gpu_goodput=g, gpu_met=met)
+    log(f"batched coarse grid: {rep}")

@@ -234,3 +234,38 @@ def test_determinism_and_range_resume():
     for k in a:
         assert np.array_equal(a[k][s], c[k]), k
     assert np.array_equal(ga[117:211], gc)
+
+
+def test_coarse_grid_ties_many_small_replicas():
+    """Hundreds of small replicas on a coarse time grid with tiny integer
+    physics and transfers of zero (simultaneous arrivals, releases exactly at
+    an arrival, equal costs), every policy and backlog mode: every replica
+    is checked against the oracle."""
+    rng = np.random.default_rng(92)
+    pols = [("learned", "true"), ("learned", "proxy"), ("round_robin", "true"), ("least_loaded", "true"),
+            ("learned_sampled", "true"), ("learned_sampled", "proxy"), ("length_threshold", "true")]
+    pts = []
+    for k in range(14):
+        pol, mode = pols[k % len(pols)]
+        pt = W.make_point(int(rng.integers(1, 4)), int(rng.integers(1, 4)), n_classes=2, policy=pol,
+                          backlog_mode=mode, len_threshold=3)
+        pt.update(pre_base_ns=int(rng.choice([0, 4])), pre_tok_ns=int(rng.choice([1, 2])),
+                  dec_tok_ns=int(rng.choice([1, 3])), xfer_tok_ns=int(rng.choice([0, 1])))
+        pts.append(pt)
+    n_rep = 480
+    lengths = rng.integers(1, 41, n_rep)
+    parts = {k: [] for k in ("arrival_ns", "prompt_len", "out_len", "pred_out_len", "slo_class")}
+    for n in lengths:
+        parts["arrival_ns"].append(np.sort(rng.integers(0, 12, n)).astype(np.int64) * 4)
+        parts["prompt_len"].append(rng.integers(1, 5, n).astype(np.int32))
+        parts["out_len"].append(rng.integers(1, 5, n).astype(np.int32))
+        parts["pred_out_len"].append(rng.integers(1, 6, n).astype(np.int32))
+        parts["slo_class"].append(rng.integers(0, 2, n).astype(np.uint8))
+    tr = {k: np.concatenate(v) for k, v in parts.items()}
+    tr["offsets"] = np.concatenate(([0], np.cumsum(lengths))).astype(np.int64)
+    tr["param_point"] = (np.arange(n_rep) % len(pts)).astype(np.int32)
+    W.add_sample_words(tr, 92)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    rep = follow_replicas(pts, tr, gpu, range(n_rep), gpu_goodput=g, gpu_met=met)
+    log(f"serial coarse grid: {rep}")
