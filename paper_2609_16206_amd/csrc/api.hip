@@ -364,6 +364,30 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
       }
     }
   }
+  // With fewer waves than SIMDs, spread the replicas out: doubling the
+  // segment width of every one-instance-per-lane class (the extra lanes
+  // idle) halves the replicas in each wave, and a wave's step costs as much
+  // as its slowest replica's step.  Widen while the waves keep growing and
+  // still fit one per SIMD.
+  if (!many) {
+    for (;;) {
+      std::vector<int> wider(choice);
+      double w2 = 0.0, w1 = 0.0;
+      for (size_t k = 0; k < npts; ++k) {
+        if (reps_of[k] == 0) continue;
+        const rt::SimClass sc = rt::sim_class(choice[k]);
+        w1 += std::ceil((double)reps_of[k] * sc.S / 64.0);
+        if ((sc.kind == rt::kSeg || sc.kind == rt::kBat) && sc.MP == 1 && sc.S < 64)
+          for (int c : sim->point_classes[k]) {
+            const rt::SimClass wc = rt::sim_class(c);
+            if (wc.kind == sc.kind && wc.mode == sc.mode && wc.MP == 1 && wc.S == 2 * sc.S) wider[k] = c;
+          }
+        w2 += std::ceil((double)reps_of[k] * rt::sim_class(wider[k]).S / 64.0);
+      }
+      if (!(w2 > w1 && w2 <= kSimds)) break;
+      choice.swap(wider);
+    }
+  }
   std::vector<std::vector<int32_t>> buckets(ncls);
   for (int64_t i = 0; i < n; ++i)
     if (off[i + 1] > off[i]) buckets[choice[pp[i]]].push_back((int32_t)i);
