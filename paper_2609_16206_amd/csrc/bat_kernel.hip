@@ -535,6 +535,20 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
   const double beta = isP ? pt.beta_pre : pt.beta_dec;
   const double xfer = (double)pt.xfer_tok_ns;
   const bool samp = pt.policy == kPolicyLearnedSampled;
+  // The point's parameters, read once: the loop's stores could alias them,
+  // so reads inside it would be repeated, each with a wait for every memory
+  // access still outstanding.
+  const int32_t ncls = pt.n_classes, pol = pt.policy, len_thr = pt.len_thr, bmode = pt.mode;
+  const float w_b = pt.w_b, w_s = pt.w_s, w_q = pt.w_q, rho = pt.rho;
+  const float tau_pre = pt.tau_pre, tau_dec = pt.tau_dec, pre_base = pt.pre_base;
+  const float inv = isP ? pt.inv_cap_pre : pt.inv_cap_dec;
+  const double pre_base_ns = (double)pt.pre_base_ns, pre_tok_ns = (double)pt.pre_tok_ns;
+  const double dec_tok_ns = (double)pt.dec_tok_ns;
+  // sigma per class of each segment's point (LDS)
+  __shared__ float sig[(kBlock / S) * kMaxClasses];
+  const int sblk = (int)(threadIdx.x / S);
+  for (int k = sl; k < kMaxClasses; k += S) sig[sblk * kMaxClasses + k] = pt.sigma[k];
+  __syncthreads();
   const int32_t C = b.C;
   Entry* const ring = reinterpret_cast<Entry*>(b.ring) + gl * (int64_t)C;
   Entry* const wring = reinterpret_cast<Entry*>(b.wring) + gl * (int64_t)C;
@@ -692,7 +706,7 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
             left = left - (double)nact * dv;
           }
           tl = tj;
-          const double w = (double)(orr - 1) * (double)pt.dec_tok_ns;
+          const double w = (double)(orr - 1) * dec_tok_ns;
           owed = owed - w;
           const double f = v + w;
           const int32_t at = ring_put(ring, C, head, nact, f, r, btail, full);
@@ -739,7 +753,7 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
     const bool mine = t < len && !dead;
     const int64_t g = lo + t;
     const bool valid = mine && p >= 1 && o >= 1 && oh >= 1 && (int64_t)p + o <= INT32_MAX &&
-                       (int64_t)p + oh <= INT32_MAX && (int32_t)c < pt.n_classes && arr >= 0 && arr >= last;
+                       (int64_t)p + oh <= INT32_MAX && (int32_t)c < ncls && arr >= 0 && arr >= last;
     if (mine && !valid) {
       rej = true;
       if (sl == 0) {
@@ -774,33 +788,31 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
     if (valid && (isP || isD)) {
       const int32_t n = isP ? P : D;
       const int32_t jj = isP ? sl : dme;
-      const int32_t pol = pt.policy;
       if (pol == kPolicyRoundRobin) {
         key = jj == t % n ? 0u : 1u;
       } else if (pol == kPolicyLeastLoaded) {
         key = (uint32_t)q;
       } else if (pol == kPolicyLengthThreshold) {
-        const bool part = isP || n == 1 || ((jj >= (n + 1) / 2) == (oh >= pt.len_thr));
+        const bool part = isP || n == 1 || ((jj >= (n + 1) / 2) == (oh >= len_thr));
         key = part ? (uint32_t)q : 0xffffffffu;
       } else {
-        const float sg = pt.sigma[c];
-        const float work = isP ? pt.w_s * (float)p * pt.tau_pre : pt.w_s * (float)oh * pt.tau_dec;
+        const float sg = sig[sblk * kMaxClasses + (int)(c & (kMaxClasses - 1))];
+        const float work = isP ? w_s * (float)p * tau_pre : w_s * (float)oh * tau_dec;
         const double need = isP ? (double)p : (double)p + (double)oh;
-        const float inv = isP ? pt.inv_cap_pre : pt.inv_cap_dec;
         float bl;
-        if (pt.mode == 0) {
+        if (bmode == 0) {
           double w = left < 0.0 ? 0.0 : left;
           w = w + owed;
           bl = (float)w * 1e-9f;
         } else if (isP) {
-          bl = pt.tau_pre * (float)pend + pt.pre_base * (float)q;
+          bl = tau_pre * (float)pend + pre_base * (float)q;
         } else {
-          bl = pt.tau_dec * (float)pend;
+          bl = tau_dec * (float)pend;
         }
         const float press = (float)(kv + need) * inv;
-        const float load = pt.w_b * bl * sg;
-        const float size = work * (1.0f + pt.rho * press) * sg;
-        key = cost_key(load + size + pt.w_q * (float)q);
+        const float load = w_b * bl * sg;
+        const float size = work * (1.0f + rho * press) * sg;
+        key = cost_key(load + size + w_q * (float)q);
         if (pol == kPolicyLearnedSampled) {
           const uint32_t u = isP ? ws.x : ws.z, w2 = isP ? ws.y : ws.w;
           const uint32_t c1 = __umulhi(u, (uint32_t)n);
@@ -821,7 +833,7 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
         a.i_dec[g] = id;
       }
       if (isP && sl == ip) {
-        const double w = (double)pt.pre_base_ns + (double)p * (double)pt.pre_tok_ns;
+        const double w = pre_base_ns + (double)p * pre_tok_ns;
         const double f = v + w;
         const int32_t at = ring_put(ring, C, head, nact, f, t, btail, full);
         if (at >= 0) {
@@ -841,7 +853,7 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
         }
       }
       if (isD && dme == id) {
-        owed = owed + (double)(o - 1) * (double)pt.dec_tok_ns;
+        owed = owed + (double)(o - 1) * dec_tok_ns;
         q += 1;
         kv = kv + ((double)p + (double)o);
         pend = pend + (double)oh;
