@@ -233,7 +233,8 @@ typedef struct {
  * The call reads offsets and param_point back to the host to plan the launch
  * (it synchronizes `hip_stream` for that), validates them (RT_EINVAL), then
  * enqueues the simulation on `hip_stream` and returns.  Scratch memory grows
- * with n_requests (80 bytes per request, for serial points), and for
+ * with n_requests (for serial points: 64 bytes per request, 128 for points
+ * with the proxy backlog, 192 when a call holds both kinds), and for
  * batched replicas with about 68 + 32 batch_cap bytes per instance slot: a
  * replica of a point with P + D <= 64 takes S slots, S the smallest of 4, 8,
  * 16, 32, 64 that holds P + D; a larger point takes P + D slots (each kind

@@ -397,21 +397,28 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
     });
 
   hipError_t e;
-  // Scratch of the serial classes: the dummy records, then the successor
-  // records (kRecStride bytes each).
-  bool any_serial = false;
+  // Scratch of the serial classes: for each record size in use (32 bytes,
+  // or 64 for the classes that price the ledger) a plane per pool, each its
+  // dummy records followed by one record per request, 256-byte aligned.
+  // Classes of one call run side by side, so each size has planes of its own.
+  bool any_serial = false, any_ledger = false, any_plain = false;
   std::vector<int> bat_classes;
   for (int c = 0; c < ncls; ++c) {
     if (buckets[c].empty()) continue;
-    if (rt::sim_class(c).kind == rt::kBat)
+    if (rt::sim_class(c).kind == rt::kBat) {
       bat_classes.push_back(c);
-    else
+    } else {
       any_serial = true;
+      (rt::mode_ledger(rt::sim_class(c).mode) ? any_ledger : any_plain) = true;
+    }
   }
   const size_t nreq = (size_t)trace->n_requests;
-  const size_t dummy_bytes = (size_t)rt::kDummyRecords * rt::kRecStride;
-  static_assert(((size_t)rt::kDummyRecords * rt::kRecStride) % 256 == 0, "records stay 256-byte aligned");
-  const size_t need = any_serial ? nreq * rt::kRecStride + dummy_bytes + 256 : 0;
+  static_assert(((size_t)rt::kDummyRecords << rt::rec_shift(false)) % 256 == 0, "planes start 256-byte aligned");
+  auto plane_bytes = [&](bool ledger) {
+    return (((nreq + rt::kDummyRecords) << rt::rec_shift(ledger)) + 255) / 256 * 256;
+  };
+  const size_t plain_plane = any_plain ? plane_bytes(false) : 0, ledger_plane = any_ledger ? plane_bytes(true) : 0;
+  const size_t need = any_serial ? 2 * plain_plane + 2 * ledger_plane + 256 : 0;
   if (need > sim->scratch_bytes) {
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
     if (sim->d_scratch) (void)hipFree(sim->d_scratch);
@@ -507,7 +514,14 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   a.i_dec = out->i_dec;
   a.ttft = out->ttft_ns;
   a.span = out->decode_span_ns;
-  a.rec = sc ? sc + dummy_bytes : nullptr;
+  // record planes by record size: index 0 of each pool's plane
+  char* rec_planes[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
+  for (int k = 0; k < 2 && sc; ++k) {
+    if (any_plain) rec_planes[0][k] = sc + k * plain_plane + ((size_t)rt::kDummyRecords << rt::rec_shift(false));
+    if (any_ledger)
+      rec_planes[1][k] = sc + 2 * plain_plane + k * ledger_plane + ((size_t)rt::kDummyRecords << rt::rec_shift(true));
+  }
+  a.rec[0] = a.rec[1] = nullptr;
   a.flag = sim->d_flag;
   if (sim->timing) {
     if ((st = collect_timing(sim)) != RT_OK) return st;
@@ -540,6 +554,9 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
     const int c = act[k];
     a.work = sim->d_work + start[c];
     a.n_work = (int64_t)buckets[c].size();
+    const int lg = rt::mode_ledger(rt::sim_class(c).mode) ? 1 : 0;
+    a.rec[0] = rec_planes[lg][0];
+    a.rec[1] = rec_planes[lg][1];
     hipStream_t where = stream;
     if (act.size() > 1) {
       where = sim->lanes[k];

@@ -52,24 +52,24 @@ struct SimArgs {
   int32_t* i_dec;
   int64_t* ttft;
   int64_t* span;
-  // Successor records of the per-instance FIFOs: kRecStride bytes per
-  // request, indexed by the global request index of the predecessor (see
-  // the offsets below).  kDummyRecords more records lie right before `rec`,
-  // at indices -1 .. -kDummyRecords: wave-private targets of record loads
-  // with nothing to load.
-  char* rec;
+  // Successor records of the per-instance FIFOs, one plane per pool
+  // (0 prefill, 1 decode), indexed by the global request index of the
+  // predecessor.  Record x holds x's first and second successor in the same
+  // instance's FIFO, each {release time (double), index, cache tokens}: one
+  // aligned 32-byte sector.  The modes that price the ledger use 64-byte
+  // records that hold the same successors' ledger tokens after the pair, so
+  // that a release reads one line (rec_shift).  Every plane has
+  // kDummyRecords more records right before its index 0, at indices
+  // -1 .. -kDummyRecords: wave-private targets of record loads and stores
+  // with nothing to do.
+  char* rec[2];
   uint32_t* flag;
 };
 
-// Layout of one request's scratch region.  For each pool, a pair of entries
-// {release time (double), index, cache tokens} describing the request's
-// first and second successor in the same instance's FIFO, and a pair of the
-// same successors' ledger tokens.
-constexpr int kRecStride = 80;
-constexpr int kRecPairPre = 0;   // 2 x 16 bytes
-constexpr int kRecPairDec = 32;  // 2 x 16 bytes
-constexpr int kRecTokPre = 64;   // 2 x 4 bytes
-constexpr int kRecTokDec = 72;   // 2 x 4 bytes
+// Record x of a plane lies at byte x << rec_shift(ledger) from its index 0;
+// in the ledger modes the two ledger tokens follow the pair at kRecTok.
+constexpr int rec_shift(bool ledger) { return ledger ? 6 : 5; }
+constexpr int kRecTok = 32;
 
 constexpr int kDummyRecords = 1024;  // a power of two
 

@@ -32,9 +32,10 @@
 // FIFO of in-flight requests per instance.  Service is in admission order,
 // so an instance releases its requests in admission order.  The first three
 // requests of each FIFO are kept in registers; the rest is a list in HBM
-// scratch in which every request's region holds its first and second
-// successor (release time, index, cache tokens; ledger tokens beside them),
-// written when those successors are admitted.  Up to two releases per
+// scratch in which every request's record holds its first and second
+// successor (release time, index, cache tokens: one 32-byte sector; ledger
+// tokens after them in the modes that price the ledger), written when those
+// successors are admitted.  Up to two releases per
 // instance between two arrivals shift the register window, and the new
 // head's two successors are then loaded with one independent access (no
 // chain of dependent loads), merged at the end of the step; a third release
@@ -124,24 +125,20 @@ __device__ __forceinline__ void pin_window(const Slot& s) {
                : "memory");
 }
 
-// Byte offset of request g's record region, g * kRecStride: g * 5 in one
-// 64-bit shift-add (written out, since the compiler would otherwise turn it
-// into two 32-bit multiply-adds), then * 16, which folds into the address
-// add.
+// Byte offset of request g's record in its pool's plane (a shift that folds
+// into the address add).
+template <bool kTok>
 __device__ __forceinline__ int64_t rec_off(int64_t g) {
-  static_assert(kRecStride == 80, "rec_off assumes 80-byte records");
-  int64_t g5;
-  asm("v_lshl_add_u64 %0, %1, 2, %1" : "=v"(g5) : "v"(g));
-  return g5 << 4;
+  return g << rec_shift(kTok);
 }
 
 template <bool kTok>
-__device__ __forceinline__ void load_pair(Slot& s, const char* rp, const char* tp) {
+__device__ __forceinline__ void load_pair(Slot& s, const char* rp) {
   const EntryPair e = *reinterpret_cast<const EntryPair*>(rp);
   s.l1 = Elem{e.a.t, e.a.idx, e.a.fp, e.a.fp};
   s.l2 = Elem{e.b.t, e.b.idx, e.b.fp, e.b.fp};
   if constexpr (kTok) {
-    const int2 k = *reinterpret_cast<const int2*>(tp);
+    const int2 k = *reinterpret_cast<const int2*>(rp + kRecTok);
     s.l1.pt = k.x;
     s.l2.pt = k.y;
   }
@@ -188,8 +185,8 @@ __device__ __forceinline__ void sample_pair(uint32_t u, uint32_t v, uint32_t n, 
 // new head's successors are loaded unconditionally (the wave's dummy record
 // `dmy` when there is nothing to load) and merged later.
 template <bool kTok, bool kKv>
-__device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char* recb, const char* tokb, int64_t base,
-                                             int32_t R, int64_t dmy) {
+__device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char* recb, int64_t base, int32_t R,
+                                             int64_t dmy) {
   const bool p1 = x.h.t <= now_eff;
   const bool p2 = x.n.t <= now_eff;  // implies p1 (release times do not decrease)
   x.q -= (p1 ? 1 : 0) + (p2 ? 1 : 0);
@@ -204,16 +201,15 @@ __device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char
   const int32_t lq = opaque(p1 ? x.q : 0);
   const bool ld = lq >= 2;
   const int64_t g = ld ? base + min(max(x.h.idx, 0), max(R - 1, 0)) : dmy;
-  const int64_t go = rec_off(g);
-  load_pair<kTok>(x, recb + go, tokb + go);
+  load_pair<kTok>(x, recb + rec_off<kTok>(g));
   x.lq = lq;
 }
 
 template <int M, bool kTok, bool kKv>
-__device__ __forceinline__ void release_fast(Slot (&s)[M], double now_eff, const char* recb, const char* tokb,
-                                             int64_t base, int32_t R, int64_t dmy) {
+__device__ __forceinline__ void release_fast(Slot (&s)[M], double now_eff, const char* recb, int64_t base, int32_t R,
+                                             int64_t dmy) {
 #pragma unroll
-  for (int m = 0; m < M; ++m) release_slot<kTok, kKv>(s[m], now_eff, recb, tokb, base, R, dmy);
+  for (int m = 0; m < M; ++m) release_slot<kTok, kKv>(s[m], now_eff, recb, base, R, dmy);
 }
 
 template <int M>
@@ -239,13 +235,13 @@ __device__ __forceinline__ double third_min(const Slot (&s)[M]) {
 // of the wave has finished after the fast releases): wait for the loaded
 // successors and release again, until no head of the wave has finished.
 template <int M, bool kTok, bool kKv>
-__device__ __forceinline__ void release_more(bool more, Slot (&s)[M], double now_eff, const char* recb,
-                                             const char* tokb, int64_t base, int32_t R, int64_t dmy) {
+__device__ __forceinline__ void release_more(bool more, Slot (&s)[M], double now_eff, const char* recb, int64_t base,
+                                             int32_t R, int64_t dmy) {
   if (__builtin_expect(more, 0)) {
     do {
 #pragma unroll
       for (int m = 0; m < M; ++m) merge_pending(s[m]);
-      release_fast<M, kTok, kKv>(s, now_eff, recb, tokb, base, R, dmy);
+      release_fast<M, kTok, kKv>(s, now_eff, recb, base, R, dmy);
     } while (__any(head_min(s) <= now_eff));
   }
 }
@@ -281,17 +277,16 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   const float basec = isp ? pt.pre_base : 0.0f;  // proxy ledger: base per in-flight prefill
   const double pre_base_ns = (double)pt.pre_base_ns, pre_tok_ns = (double)pt.pre_tok_ns;
   const double dec_tok_ns = (double)pt.dec_tok_ns, xfer_tok_ns = (double)pt.xfer_tok_ns;
-  char* const recb = a.rec + (isp ? kRecPairPre : kRecPairDec);
-  char* const tokb = a.rec + (isp ? kRecTokPre : kRecTokDec);
-  // The wave's dummy record: a negative request index whose region lies in
-  // the dummy area just before the records.  Record loads and stores with
+  char* const recb = isp ? a.rec[0] : a.rec[1];
+  // The wave's dummy record: a negative request index whose records lie in
+  // the dummy areas just before the planes.  Record loads and stores with
   // nothing to do use it, so that only an index is selected; output stores
-  // with nothing to write go to its first 24 bytes.  (Stores stay
+  // with nothing to write go to the first 24 bytes of its prefill record.  (Stores stay
   // unconditional: each lane of a store sends its own L2 request, but
   // switching exec off and on around the store costs more issue time here.)
   const uint32_t wave_id = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) & (kDummyRecords - 1);
   const int64_t dmy = -1 - (int64_t)wave_id;
-  char* const dummy = a.rec + dmy * kRecStride;
+  char* const dummy = a.rec[0] + rec_off<kTok>(dmy);
 
   // sigma per class of each segment's point, read a step ahead of its use
   __shared__ float sig[kWaves * kSegs * kMaxClasses];
@@ -462,12 +457,13 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
       const Entry ze{end, t, fp};
       const bool s1 = opaque(st1) >= 0, s2 = opaque(st2) >= 0;
       const int64_t g1 = s1 ? base + st1 : dmy, g2 = s2 ? base + st2 : dmy;
-      const int64_t o1 = rec_off(g1), o2 = rec_off(g2);
-      *reinterpret_cast<Entry*>(recb + o1) = ze;
-      *reinterpret_cast<Entry*>(recb + o2 + 16) = ze;
+      char* const r1 = recb + rec_off<kTok>(g1);
+      char* const r2 = recb + rec_off<kTok>(g2);
+      *reinterpret_cast<Entry*>(r1) = ze;
+      *reinterpret_cast<Entry*>(r2 + 16) = ze;
       if constexpr (kTok) {
-        *reinterpret_cast<int32_t*>(tokb + o1) = tk;
-        *reinterpret_cast<int32_t*>(tokb + o2 + 4) = tk;
+        *reinterpret_cast<int32_t*>(r1 + kRecTok) = tk;
+        *reinterpret_cast<int32_t*>(r2 + kRecTok + 4) = tk;
       }
       const int64_t go_i = base + t;
       int32_t* const d_ip = own_out ? a.i_pre + go_i : reinterpret_cast<int32_t*>(dummy);
@@ -504,8 +500,8 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     cu = nx.u;
     cv = nx.v;
     const bool more = __any(third_min(s) <= cur.now_eff);
-    release_fast<M, kTok, kKv>(s, cur.now_eff, recb, tokb, base, R, dmy);
-    release_more<M, kTok, kKv>(more, s, cur.now_eff, recb, tokb, base, R, dmy);
+    release_fast<M, kTok, kKv>(s, cur.now_eff, recb, base, R, dmy);
+    release_more<M, kTok, kKv>(more, s, cur.now_eff, recb, base, R, dmy);
     load_feat(ld, t + 2);
   };
 

@@ -65,8 +65,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   const float basec = isp ? pt.pre_base : 0.0f;  // proxy ledger: base per in-flight prefill
   const double pre_base_ns = (double)pt.pre_base_ns, pre_tok_ns = (double)pt.pre_tok_ns;
   const double dec_tok_ns = (double)pt.dec_tok_ns, xfer_tok_ns = (double)pt.xfer_tok_ns;
-  char* const recb = a.rec + (isp ? kRecPairPre : kRecPairDec);
-  char* const tokb = a.rec + (isp ? kRecTokPre : kRecTokDec);
+  char* const recb = isp ? a.rec[0] : a.rec[1];
   const uint32_t wave_id = (blockIdx.x * W + wave) & (kDummyRecords - 1);
   const int64_t dmy = -1 - (int64_t)wave_id;  // the wave's dummy record
 
@@ -266,11 +265,11 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           if constexpr (kTok) x.pend = x.pend + (own ? (double)p : 0.0);
           x.busy = own ? pf_end : x.busy;
           if constexpr (kTok) {
-            store_x4_b32_if(s1, recb + rec_off(g1), zv, tokb + rec_off(g1), (uint32_t)p);
-            store_x4_b32_if(s2, recb + rec_off(g2) + 16, zv, tokb + rec_off(g2) + 4, (uint32_t)p);
+            store_x4_b32_if(s1, recb + rec_off<kTok>(g1), zv, recb + rec_off<kTok>(g1) + kRecTok, (uint32_t)p);
+            store_x4_b32_if(s2, recb + rec_off<kTok>(g2) + 16, zv, recb + rec_off<kTok>(g2) + kRecTok + 4, (uint32_t)p);
           } else {
-            store_x4_if(s1, recb + rec_off(g1), zv);
-            store_x4_if(s2, recb + rec_off(g2) + 16, zv);
+            store_x4_if(s1, recb + rec_off<kTok>(g1), zv);
+            store_x4_if(s2, recb + rec_off<kTok>(g2) + 16, zv);
           }
         }
     }
@@ -296,11 +295,11 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           x.busy = own ? de : x.busy;
           const u32x4 zv = {(uint32_t)__double2loint(de), (uint32_t)__double2hiint(de), (uint32_t)t, (uint32_t)po};
           if constexpr (kTok) {
-            store_x4_b32_if(s1, recb + rec_off(g1), zv, tokb + rec_off(g1), (uint32_t)oh);
-            store_x4_b32_if(s2, recb + rec_off(g2) + 16, zv, tokb + rec_off(g2) + 4, (uint32_t)oh);
+            store_x4_b32_if(s1, recb + rec_off<kTok>(g1), zv, recb + rec_off<kTok>(g1) + kRecTok, (uint32_t)oh);
+            store_x4_b32_if(s2, recb + rec_off<kTok>(g2) + 16, zv, recb + rec_off<kTok>(g2) + kRecTok + 4, (uint32_t)oh);
           } else {
-            store_x4_if(s1, recb + rec_off(g1), zv);
-            store_x4_if(s2, recb + rec_off(g2) + 16, zv);
+            store_x4_if(s1, recb + rec_off<kTok>(g1), zv);
+            store_x4_if(s2, recb + rec_off<kTok>(g2) + 16, zv);
           }
           // the outcome, by the decode winner
           tmax = __builtin_fmax(tmax, own ? de : 0.0);
@@ -330,9 +329,9 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
       for (int m = 0; m < M; ++m) any_done[m] = __ballot(s[m].h.t <= cur.now_eff);
 #pragma unroll
       for (int m = 0; m < M; ++m)
-        if (any_done[m]) release_slot<kTok, kKv>(s[m], cur.now_eff, recb, tokb, base, R, dmy);
+        if (any_done[m]) release_slot<kTok, kKv>(s[m], cur.now_eff, recb, base, R, dmy);
     }
-    release_more<M, kTok, kKv>(__any(head_min(s) <= cur.now_eff), s, cur.now_eff, recb, tokb, base, R, dmy);
+    release_more<M, kTok, kKv>(__any(head_min(s) <= cur.now_eff), s, cur.now_eff, recb, base, R, dmy);
     {
       const int64_t g = base + min(t + 2, last);
       nx_arr = a.arrival[g];
