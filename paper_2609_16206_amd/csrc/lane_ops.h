@@ -197,6 +197,35 @@ __device__ __forceinline__ double seg_bcast_f64(double v, bool own, int lane) {
   return __hiloint2double((int)hi, (int)lo);
 }
 
+// Two broadcasts at once: x from the lane of each segment where `ox` holds and
+// y from the one where `oy` holds, the four halves reduced interleaved.
+template <int S>
+__device__ __forceinline__ void seg_bcast2_f64(double& x, bool ox, double& y, bool oy, int lane) {
+  uint32_t a = ox ? (uint32_t)__double2loint(x) : 0u, b = ox ? (uint32_t)__double2hiint(x) : 0u;
+  uint32_t c = oy ? (uint32_t)__double2loint(y) : 0u, d = oy ? (uint32_t)__double2hiint(y) : 0u;
+  if constexpr (S >= 2) { a |= dpp<0xB1>(a); b |= dpp<0xB1>(b); c |= dpp<0xB1>(c); d |= dpp<0xB1>(d); }
+  if constexpr (S >= 4) { a |= dpp<0x4E>(a); b |= dpp<0x4E>(b); c |= dpp<0x4E>(c); d |= dpp<0x4E>(d); }
+  if constexpr (S >= 8) { a |= dpp<0x141>(a); b |= dpp<0x141>(b); c |= dpp<0x141>(c); d |= dpp<0x141>(d); }
+  if constexpr (S >= 16) { a |= dpp<0x140>(a); b |= dpp<0x140>(b); c |= dpp<0x140>(c); d |= dpp<0x140>(d); }
+  if constexpr (S == 32) {
+    const uint32_t a0 = rl(a, 0) | rl(a, 16), a1 = rl(a, 32) | rl(a, 48);
+    const uint32_t b0 = rl(b, 0) | rl(b, 16), b1 = rl(b, 32) | rl(b, 48);
+    const uint32_t c0 = rl(c, 0) | rl(c, 16), c1 = rl(c, 32) | rl(c, 48);
+    const uint32_t d0 = rl(d, 0) | rl(d, 16), d1 = rl(d, 32) | rl(d, 48);
+    a = lane < 32 ? a0 : a1;
+    b = lane < 32 ? b0 : b1;
+    c = lane < 32 ? c0 : c1;
+    d = lane < 32 ? d0 : d1;
+  } else if constexpr (S >= 64) {
+    a = (rl(a, 0) | rl(a, 16)) | (rl(a, 32) | rl(a, 48));
+    b = (rl(b, 0) | rl(b, 16)) | (rl(b, 32) | rl(b, 48));
+    c = (rl(c, 0) | rl(c, 16)) | (rl(c, 32) | rl(c, 48));
+    d = (rl(d, 0) | rl(d, 16)) | (rl(d, 32) | rl(d, 48));
+  }
+  x = __hiloint2double((int)b, (int)a);
+  y = __hiloint2double((int)d, (int)c);
+}
+
 // Lowest lane (relative to the segment, or to the wave for S >= 64) of each
 // segment where `pred` holds; -1 where it holds nowhere.
 template <int S>

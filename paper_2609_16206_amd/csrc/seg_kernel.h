@@ -280,13 +280,11 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   char* const recb = isp ? a.rec[0] : a.rec[1];
   // The wave's dummy record: a negative request index whose records lie in
   // the dummy areas just before the planes.  Record loads and stores with
-  // nothing to do use it, so that only an index is selected; output stores
-  // with nothing to write go to the first 24 bytes of its prefill record.  (Stores stay
+  // nothing to do use it, so that only an index is selected.  (Stores stay
   // unconditional: each lane of a store sends its own L2 request, but
   // switching exec off and on around the store costs more issue time here.)
   const uint32_t wave_id = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) & (kDummyRecords - 1);
   const int64_t dmy = -1 - (int64_t)wave_id;
-  char* const dummy = a.rec[0] + rec_off<kTok>(dmy);
 
   // sigma per class of each segment's point, read a step ahead of its use
   __shared__ float sig[kWaves * kSegs * kMaxClasses];
@@ -331,6 +329,23 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
       f.v = w.y;
     } else {
       f.u = f.v = 0;
+    }
+  };
+
+  // Outcomes of the current block of S steps: lane k of a segment keeps
+  // step (block start + k)'s, and the block is written with one coalesced
+  // store per output array (a per-step store would send one write request
+  // per lane of the wave, mostly to a dummy slot).
+  int32_t b_ip = -1, b_id = -1;
+  int64_t b_tt = -1, b_sp = -1;
+  auto flush = [&](int32_t t0) {
+    const int32_t tl = t0 + sl;
+    if (tl < R) {
+      const int64_t gi = base + tl;
+      a.i_pre[gi] = b_ip;
+      a.i_dec[gi] = b_id;
+      a.ttft[gi] = b_tt;
+      a.span[gi] = b_sp;
     }
   };
 
@@ -413,10 +428,14 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     const int32_t id = (wd - LP) * M + md;
 
     // 3. serve: prefill, KV transfer, decode (exact integers in doubles)
+    // (the winners' busy-until, broadcast over the segment, so that every
+    // lane forms both ends)
+    double busy_p = bbusy, busy_d = bbusy;
+    seg_bcast2_f64<S>(busy_p, sl == wp, busy_d, sl == wd, lane);
     const double s_pre = __builtin_fma((double)p, pre_tok_ns, pre_base_ns);
-    const double pf_end = seg_bcast_f64<S>(__builtin_fmax(now, bbusy) + s_pre, sl == wp, lane);
+    const double pf_end = __builtin_fmax(now, busy_p) + s_pre;
     const double kv_at = pf_end + (double)p * xfer_tok_ns;
-    const double de = __builtin_fmax(kv_at, bbusy) + (double)(o - 1) * dec_tok_ns;  // on the decode winner
+    const double de = __builtin_fmax(kv_at, busy_d) + (double)(o - 1) * dec_tok_ns;
     const double end = isp ? pf_end : de;
     const int32_t fp = isp ? p : po;  // cache tokens held until release
     const int32_t tk = isp ? p : oh;  // ledger tokens
@@ -443,17 +462,20 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
       x.busy = own ? end : x.busy;
     }
 
-    // 4. the outcome, written by the decode winner (lane 0 of the segment for
-    // a rejected request); the records of z; every lane stores (the ones
-    // with nothing to store address the dummies)
+    // 4. the outcome, kept by lane t mod S of the segment until the block's
+    // flush; the records of z, stored by every lane (the ones with nothing to
+    // store address the dummies)
     {
-      const int32_t ow = opaque((R - t) >= 1 ? (go ? wd : 0) : -1);
-      const bool own_out = ow == sl;
       const int32_t o_ip = go ? ip : -1, o_id = go ? id : -1;
       const int64_t o_ttft = go ? f64_to_i64(pf_end - now) : -1;
       const int64_t o_span = go ? f64_to_i64(de - pf_end) : -1;
+      const bool keep = opaque(t & (S - 1)) == sl;
+      b_ip = keep ? o_ip : b_ip;
+      b_id = keep ? o_id : b_id;
+      b_tt = keep ? o_ttft : b_tt;
+      b_sp = keep ? o_span : b_sp;
       tmax = __builtin_fmax(tmax, opaque(opaque(go ? wd : -1) == sl ? de : 0.0));
-      rej |= opaque(go ? 0u : 1u) & opaque(own_out ? 1u : 0u);
+      rej |= opaque(go ? 0u : 1u) & opaque((R - t) >= 1 && sl == 0 ? 1u : 0u);
       const Entry ze{end, t, fp};
       const bool s1 = opaque(st1) >= 0, s2 = opaque(st2) >= 0;
       const int64_t g1 = s1 ? base + st1 : dmy, g2 = s2 ? base + st2 : dmy;
@@ -465,15 +487,6 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
         *reinterpret_cast<int32_t*>(r1 + kRecTok) = tk;
         *reinterpret_cast<int32_t*>(r2 + kRecTok + 4) = tk;
       }
-      const int64_t go_i = base + t;
-      int32_t* const d_ip = own_out ? a.i_pre + go_i : reinterpret_cast<int32_t*>(dummy);
-      int32_t* const d_id = own_out ? a.i_dec + go_i : reinterpret_cast<int32_t*>(dummy + 4);
-      int64_t* const d_tt = own_out ? a.ttft + go_i : reinterpret_cast<int64_t*>(dummy + 8);
-      int64_t* const d_sp = own_out ? a.span + go_i : reinterpret_cast<int64_t*>(dummy + 16);
-      *d_ip = o_ip;
-      *d_id = o_id;
-      *d_tt = o_ttft;
-      *d_sp = o_span;
     }
     if constexpr (kMode == kModeBase) rr = (rr + 1 == npool) ? 0 : rr + 1;
 
@@ -522,11 +535,16 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   // read in the next from the same registers
   // (the count of steps left is a scalar, so the loop tests read no vector
   // register)
+  // (S is even, so a block ends on the second step of an iteration)
   int32_t t = 0;
   for (int32_t left = Rmax; left > 0; left -= 2, t += 2) {
     step(t, fa, fb);
-    if (left > 1) step(t + 1, fb, fa);
+    if (left > 1) {
+      step(t + 1, fb, fa);
+      if (((t + 1) & (S - 1)) == S - 1) flush((t + 1) & ~(S - 1));
+    }
   }
+  if (Rmax & (S - 1)) flush(Rmax & ~(S - 1));
   const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u);
   if (flag) atomicOr(a.flag, flag);
 }
