@@ -269,3 +269,22 @@ def test_coarse_grid_ties_many_small_replicas():
     assert flags == 0
     rep = follow_replicas(pts, tr, gpu, range(n_rep), gpu_goodput=g, gpu_met=met)
     log(f"serial coarse grid: {rep}")
+
+
+@pytest.mark.parametrize("P,D,n_rep", [(1, 1, 32768), (1, 2, 16384), (1, 1, 8192), (2, 6, 4096), (8, 8, 2048),
+                                       (16, 16, 1024)])
+def test_outcome_blocks_every_residue(P, D, n_rep):
+    """The one-wave kernels write outcomes in blocks of S steps (lane k of a
+    segment keeps step block start + k).  Replica lengths cycle through
+    1..130, so a replica's last block ends at every residue modulo the
+    segment width; the replica counts are chosen so that the planner's
+    widening stops at S = 2, 4, 8, 16, 32 and 64 in turn (one wave per SIMD)."""
+    pts = [W.make_point(P, D, n_classes=3, kv_cap=50_000)]
+    lengths = [1 + (i % 130) for i in range(n_rep)]
+    tr = _ragged_trace(pts, lengths, seed=23, rate_scale=1.2)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    check_properties(pts, tr, gpu)
+    assert np.array_equal(goodput_recount(pts, tr, gpu), met)
+    rep = follow_replicas(pts, tr, gpu, range(n_rep), gpu_goodput=g, gpu_met=met)
+    log(f"outcome blocks {P}P+{D}D x {n_rep}: {rep}")
