@@ -24,10 +24,15 @@
 // written so that every condition is a single vector compare feeding vector
 // selects (sentinels fold the conditions: a FIFO position beyond the FIFO's
 // length has release time +inf, and a rejected request uses now = -1, so
-// "the head has finished" is the one compare head <= now), and every memory
-// instruction is issued unconditionally (a lane with nothing to load or store
-// addresses its wave's dummy slot).  The only branches of a step are the
-// loop and a rare slow path.
+// "the head has finished" is the one compare head <= now), and every record
+// load and store is issued unconditionally (a lane with nothing to load or
+// store addresses its wave's dummy slot).  The only branches of a step are
+// the loop and a rare slow path.
+//
+// Outcomes.  A store sends one write request per enabled lane, wherever it
+// points, so the step does not store outcomes: lane k of a segment keeps the
+// outcome of step (block start + k), and every S steps the segment writes
+// the block with one coalesced store per output array.
 //
 // FIFO of in-flight requests per instance.  Service is in admission order,
 // so an instance releases its requests in admission order.  The first three
@@ -35,8 +40,8 @@
 // scratch in which every request's record holds its first and second
 // successor (release time, index, cache tokens: one 32-byte sector; ledger
 // tokens after them in the modes that price the ledger), written when those
-// successors are admitted.  Up to two releases per
-// instance between two arrivals shift the register window, and the new
+// successors are admitted.  Up to two releases per instance between two
+// arrivals shift the register window, and the new
 // head's two successors are then loaded with one independent access (no
 // chain of dependent loads), merged at the end of the step; a third release
 // in one step takes the slow path, which waits.
