@@ -137,6 +137,21 @@ __device__ __forceinline__ int64_t rec_off(int64_t g) {
   return g << rec_shift(kTok);
 }
 
+// Address of record g of a plane based at p.  (A single v_lshl_add_u64
+// takes shifts of 0..4 only; records are 32 or 64 bytes.)
+template <bool kTok>
+__device__ __forceinline__ char* rec_at(const char* p, int64_t g) {
+  return const_cast<char*>(p) + rec_off<kTok>(g);
+}
+
+// The 64-bit index `x` where `c` holds, else `d` (x >= 0): the two halves
+// selected apart, with no sign extension of x.
+__device__ __forceinline__ int64_t sel_index(bool c, int32_t x, int64_t d) {
+  const uint32_t lo = c ? (uint32_t)x : (uint32_t)(uint64_t)d;
+  const uint32_t hi = c ? 0u : (uint32_t)((uint64_t)d >> 32);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 template <bool kTok>
 __device__ __forceinline__ void load_pair(Slot& s, const char* rp) {
   const EntryPair e = *reinterpret_cast<const EntryPair*>(rp);
@@ -188,10 +203,11 @@ __device__ __forceinline__ void sample_pair(uint32_t u, uint32_t v, uint32_t n, 
 
 // Release: up to two completions per instance from the register window; the
 // new head's successors are loaded unconditionally (the wave's dummy record
-// `dmy` when there is nothing to load) and merged later.
+// `dmy` when there is nothing to load) and merged later.  `recr` is the
+// lane's record plane at its replica's request 0; indices are relative to
+// it (the dummy's too), so that an address is one shift-add.
 template <bool kTok, bool kKv>
-__device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char* recb, int64_t base, int32_t R,
-                                             int64_t dmy) {
+__device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char* recr, int32_t R, int64_t dmy) {
   const bool p1 = x.h.t <= now_eff;
   const bool p2 = x.n.t <= now_eff;  // implies p1 (release times do not decrease)
   x.q -= (p1 ? 1 : 0) + (p2 ? 1 : 0);
@@ -205,16 +221,15 @@ __device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char
   x.n2.t = p1 ? kInf : x.n2.t;
   const int32_t lq = opaque(p1 ? x.q : 0);
   const bool ld = lq >= 2;
-  const int64_t g = ld ? base + min(max(x.h.idx, 0), max(R - 1, 0)) : dmy;
-  load_pair<kTok>(x, recb + rec_off<kTok>(g));
+  const int64_t g = sel_index(ld, min(max(x.h.idx, 0), max(R - 1, 0)), dmy);
+  load_pair<kTok>(x, rec_at<kTok>(recr, g));
   x.lq = lq;
 }
 
 template <int M, bool kTok, bool kKv>
-__device__ __forceinline__ void release_fast(Slot (&s)[M], double now_eff, const char* recb, int64_t base, int32_t R,
-                                             int64_t dmy) {
+__device__ __forceinline__ void release_fast(Slot (&s)[M], double now_eff, const char* recr, int32_t R, int64_t dmy) {
 #pragma unroll
-  for (int m = 0; m < M; ++m) release_slot<kTok, kKv>(s[m], now_eff, recb, base, R, dmy);
+  for (int m = 0; m < M; ++m) release_slot<kTok, kKv>(s[m], now_eff, recr, R, dmy);
 }
 
 template <int M>
@@ -240,13 +255,13 @@ __device__ __forceinline__ double third_min(const Slot (&s)[M]) {
 // of the wave has finished after the fast releases): wait for the loaded
 // successors and release again, until no head of the wave has finished.
 template <int M, bool kTok, bool kKv>
-__device__ __forceinline__ void release_more(bool more, Slot (&s)[M], double now_eff, const char* recb, int64_t base,
-                                             int32_t R, int64_t dmy) {
+__device__ __forceinline__ void release_more(bool more, Slot (&s)[M], double now_eff, const char* recr, int32_t R,
+                                             int64_t dmy) {
   if (__builtin_expect(more, 0)) {
     do {
 #pragma unroll
       for (int m = 0; m < M; ++m) merge_pending(s[m]);
-      release_fast<M, kTok, kKv>(s, now_eff, recb, base, R, dmy);
+      release_fast<M, kTok, kKv>(s, now_eff, recr, R, dmy);
     } while (__any(head_min(s) <= now_eff));
   }
 }
@@ -289,7 +304,10 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
   // unconditional: each lane of a store sends its own L2 request, but
   // switching exec off and on around the store costs more issue time here.)
   const uint32_t wave_id = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) & (kDummyRecords - 1);
-  const int64_t dmy = -1 - (int64_t)wave_id;
+  // the lane's plane at its replica's request 0, and the dummy's index
+  // relative to it
+  char* const recr = recb + rec_off<kTok>(base);
+  const int64_t dmy = -1 - (int64_t)wave_id - base;
 
   // sigma per class of each segment's point, read a step ahead of its use
   __shared__ float sig[kWaves * kSegs * kMaxClasses];
@@ -483,9 +501,8 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
       rej |= opaque(go ? 0u : 1u) & opaque((R - t) >= 1 && sl == 0 ? 1u : 0u);
       const Entry ze{end, t, fp};
       const bool s1 = opaque(st1) >= 0, s2 = opaque(st2) >= 0;
-      const int64_t g1 = s1 ? base + st1 : dmy, g2 = s2 ? base + st2 : dmy;
-      char* const r1 = recb + rec_off<kTok>(g1);
-      char* const r2 = recb + rec_off<kTok>(g2);
+      char* const r1 = rec_at<kTok>(recr, sel_index(s1, st1, dmy));
+      char* const r2 = rec_at<kTok>(recr, sel_index(s2, st2, dmy));
       *reinterpret_cast<Entry*>(r1) = ze;
       *reinterpret_cast<Entry*>(r2 + 16) = ze;
       if constexpr (kTok) {
@@ -518,8 +535,8 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     cu = nx.u;
     cv = nx.v;
     const bool more = __any(third_min(s) <= cur.now_eff);
-    release_fast<M, kTok, kKv>(s, cur.now_eff, recb, base, R, dmy);
-    release_more<M, kTok, kKv>(more, s, cur.now_eff, recb, base, R, dmy);
+    release_fast<M, kTok, kKv>(s, cur.now_eff, recr, R, dmy);
+    release_more<M, kTok, kKv>(more, s, cur.now_eff, recr, R, dmy);
     load_feat(ld, t + 2);
   };
 

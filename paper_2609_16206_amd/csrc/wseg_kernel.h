@@ -67,7 +67,10 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   const double dec_tok_ns = (double)pt.dec_tok_ns, xfer_tok_ns = (double)pt.xfer_tok_ns;
   char* const recb = isp ? a.rec[0] : a.rec[1];
   const uint32_t wave_id = (blockIdx.x * W + wave) & (kDummyRecords - 1);
-  const int64_t dmy = -1 - (int64_t)wave_id;  // the wave's dummy record
+  // the lane's plane at its replica's request 0; the wave's dummy record,
+  // indexed relative to it
+  char* const recr = recb + rec_off<kTok>(base);
+  const int64_t dmy = -1 - (int64_t)wave_id - base;
 
   struct Part {
     uint32_t kp, kd;  // the wave's best prefill / decode key
@@ -241,9 +244,9 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
 
     // 6. append the request to the winning slot of each pool (uniform
     // branches: the winner's wave, the winner's slot) and record the outcome;
-    // only the lanes with something to store store it.  Addresses are valid
-    // on every lane: a tail is >= -1, and index -1 lies in the dummy area
-    // before the records.
+    // only the lanes with something to store store it.  Addresses stay inside
+    // the plane on every lane: a tail is >= -1, and index -1 is the record
+    // before the replica's first (a dummy record for the trace's first).
     if (go && wave == wpo) {
       const Elem z{pf_end, t, p, p};
       const u32x4 zv = {(uint32_t)__double2loint(pf_end), (uint32_t)__double2hiint(pf_end), (uint32_t)t, (uint32_t)p};
@@ -257,7 +260,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           x.n = sel(w == 1, z, x.n);
           x.n2 = sel(w == 2, z, x.n2);
           const uint32_t s1 = opaque(w) >= 1 ? 1u : 0u, s2 = opaque(w) >= 2 ? 1u : 0u;
-          const int64_t g1 = base + x.tail, g2 = base + x.tail2;
+          const int64_t g1 = x.tail, g2 = x.tail2;
           x.tail2 = own ? x.tail : x.tail2;
           x.tail = own ? t : x.tail;
           x.q = own ? x.q + 1 : x.q;
@@ -265,11 +268,11 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           if constexpr (kTok) x.pend = x.pend + (own ? (double)p : 0.0);
           x.busy = own ? pf_end : x.busy;
           if constexpr (kTok) {
-            store_x4_b32_if(s1, recb + rec_off<kTok>(g1), zv, recb + rec_off<kTok>(g1) + kRecTok, (uint32_t)p);
-            store_x4_b32_if(s2, recb + rec_off<kTok>(g2) + 16, zv, recb + rec_off<kTok>(g2) + kRecTok + 4, (uint32_t)p);
+            store_x4_b32_if(s1, recr + rec_off<kTok>(g1), zv, recr + rec_off<kTok>(g1) + kRecTok, (uint32_t)p);
+            store_x4_b32_if(s2, recr + rec_off<kTok>(g2) + 16, zv, recr + rec_off<kTok>(g2) + kRecTok + 4, (uint32_t)p);
           } else {
-            store_x4_if(s1, recb + rec_off<kTok>(g1), zv);
-            store_x4_if(s2, recb + rec_off<kTok>(g2) + 16, zv);
+            store_x4_if(s1, recr + rec_off<kTok>(g1), zv);
+            store_x4_if(s2, recr + rec_off<kTok>(g2) + 16, zv);
           }
         }
     }
@@ -286,7 +289,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           x.n = sel(w == 1, z, x.n);
           x.n2 = sel(w == 2, z, x.n2);
           const uint32_t s1 = opaque(w) >= 1 ? 1u : 0u, s2 = opaque(w) >= 2 ? 1u : 0u;
-          const int64_t g1 = base + x.tail, g2 = base + x.tail2;
+          const int64_t g1 = x.tail, g2 = x.tail2;
           x.tail2 = own ? x.tail : x.tail2;
           x.tail = own ? t : x.tail;
           x.q = own ? x.q + 1 : x.q;
@@ -295,11 +298,11 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           x.busy = own ? de : x.busy;
           const u32x4 zv = {(uint32_t)__double2loint(de), (uint32_t)__double2hiint(de), (uint32_t)t, (uint32_t)po};
           if constexpr (kTok) {
-            store_x4_b32_if(s1, recb + rec_off<kTok>(g1), zv, recb + rec_off<kTok>(g1) + kRecTok, (uint32_t)oh);
-            store_x4_b32_if(s2, recb + rec_off<kTok>(g2) + 16, zv, recb + rec_off<kTok>(g2) + kRecTok + 4, (uint32_t)oh);
+            store_x4_b32_if(s1, recr + rec_off<kTok>(g1), zv, recr + rec_off<kTok>(g1) + kRecTok, (uint32_t)oh);
+            store_x4_b32_if(s2, recr + rec_off<kTok>(g2) + 16, zv, recr + rec_off<kTok>(g2) + kRecTok + 4, (uint32_t)oh);
           } else {
-            store_x4_if(s1, recb + rec_off<kTok>(g1), zv);
-            store_x4_if(s2, recb + rec_off<kTok>(g2) + 16, zv);
+            store_x4_if(s1, recr + rec_off<kTok>(g1), zv);
+            store_x4_if(s2, recr + rec_off<kTok>(g2) + 16, zv);
           }
           // the outcome, by the decode winner
           tmax = __builtin_fmax(tmax, own ? de : 0.0);
@@ -329,9 +332,9 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
       for (int m = 0; m < M; ++m) any_done[m] = __ballot(s[m].h.t <= cur.now_eff);
 #pragma unroll
       for (int m = 0; m < M; ++m)
-        if (any_done[m]) release_slot<kTok, kKv>(s[m], cur.now_eff, recb, base, R, dmy);
+        if (any_done[m]) release_slot<kTok, kKv>(s[m], cur.now_eff, recr, R, dmy);
     }
-    release_more<M, kTok, kKv>(__any(head_min(s) <= cur.now_eff), s, cur.now_eff, recb, base, R, dmy);
+    release_more<M, kTok, kKv>(__any(head_min(s) <= cur.now_eff), s, cur.now_eff, recr, R, dmy);
     {
       const int64_t g = base + min(t + 2, last);
       nx_arr = a.arrival[g];
