@@ -3,9 +3,10 @@
 A step is one pass of the whole hot path over one batch of synthetic input:
 rt_sim_run_replicas (every replica: release, score both pools, argmin,
 serve, record) followed by rt_goodput (per-replica SLO attainment).  The
-default workload is the paper-shaped cluster: 4,096 replicas x 10,000
-requests, 2 prefill + 6 decode instances, mixed bursty MMPP traffic, learned
-router with the simulation-clock backlog.
+default workload is the largest single-GPU configuration, the large pool:
+256 replicas x 1,000,000 requests, 128 prefill + 1,024 decode instances,
+Poisson arrivals at 0.95 of capacity, Pareto output lengths, learned router
+with the simulation-clock backlog (294.9 G scored pairs per step).
 
 Prints one JSON line: simulated requests/s over K timed steps (inputs
 resident in HBM), the dominant kernel's roofline position measured with HIP
@@ -28,14 +29,24 @@ HBM_PEAK = 8.0e12  # B/s, MI355X HBM3E
 # Plain VALU lane-op peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (one
 # non-fused, non-packed op per lane per clock).
 ALU_PEAK = 256 * 4 * 16 * 2.4e9
-# Algorithmic work per unit (derivation in the design notes):
+# Algorithmic work per unit, as the scope analysis counts it: about 12 VALU
+# lane-ops per scored pair (int add, 2 conversions, 7 fp32 ops,
+# compare/select, the release compare) and about 40 of bookkeeping per
+# request; 10 per pair for the standalone scorer, whose backlog is given.
 SIM_BYTES_PER_REQ = 21 + 24  # trace in (i64 + 3 x i32 + u8), outputs out (2 x i32 + 2 x i64)
 SAMPLE_BYTES_PER_REQ = 16  # the sampled policy's four candidate words
-SIM_OPS_PER_PAIR = 19  # backlog 4, press 3, (1 + rho press) 2, size 2, load 2, queue 2, sums 2, argmin 1, release 1
-SIM_OPS_PER_REQ = 25  # priced work, need, service times, Lindley updates, state and outputs
+SIM_OPS_PER_PAIR = 12
+SIM_OPS_PER_REQ = 40
+SCORE_OPS_PER_PAIR = 10
+SCORE_OPS_PER_REQ = 0
+# The design notes' own recount of the written arithmetic (reported beside
+# the fraction above, labelled): backlog 4, press 3, factor 2, size 2, load 2,
+# queue 2, sums 2, argmin 1, release 1 = 19 per pair and 25 per request; the
+# scorer 14 per pair and 4 per request.
+RECOUNT_SIM = (19, 25)
+RECOUNT_SCORE = (14, 4)
 SCORE_BYTES_PER_REQ = 4 + 4 + 1 + 4 + 4  # p, o^, class in; index, score out
-SCORE_OPS_PER_PAIR = 14  # the equation with backlog given: press 3, factor 2, size 2, load 2, queue 2, sums 2, argmin 1
-SCORE_OPS_PER_REQ = 4
+SCORE_BYTES_PER_PAIR_ROWS = 4 + 4 + 4  # per-request snapshot rows: backlog, queue, occupancy
 
 
 def _workload(name):
@@ -54,6 +65,8 @@ def _workload(name):
         return W.param_sweep()
     if name == "large":
         return W.large_pool_wl()
+    if name == "batched_wide_pool":
+        return W.batched_wide_pool()
     raise SystemExit(f"unknown workload {name}")
 
 
@@ -85,9 +98,19 @@ def _traffic(kernel_tag, workload_name, sources):
     return d.get("bytes_per_launch")
 
 
+def cpu_threads():
+    """Threads for the oracle's baseline: the cores this process may run on,
+    capped by OMP_NUM_THREADS where the host sets the job's CPU share."""
+    n = len(os.sched_getaffinity(0))
+    share = os.environ.get("OMP_NUM_THREADS")
+    if share and share.isdigit() and int(share) > 0:
+        n = min(n, int(share))
+    return max(1, n)
+
+
 def _cpu_baseline_sim(wl, tr, budget_s):
     from oracle import oracle as O
-    threads = min(16, os.cpu_count() or 1)
+    threads = cpu_threads()
     off = tr["offsets"]
     n_rep = len(off) - 1
     done_req = 0
@@ -108,7 +131,8 @@ def _cpu_baseline_sim(wl, tr, budget_s):
     dt = time.perf_counter() - t0
     return dict(value=done_req / dt, unit="requests/s", cores=threads, kind="oracle",
                 pairs_per_s=pairs / dt,
-                sample=f"{done_rep} of {n_rep} replicas ({done_req} requests), {threads} threads, {dt:.1f} s")
+                sample=f"{done_rep} of {n_rep} replicas ({done_req} requests), {threads} threads "
+                       f"(affinity {len(os.sched_getaffinity(0))} cores), {dt:.1f} s")
 
 
 def bench_sim(args):
@@ -165,11 +189,15 @@ def bench_sim(args):
     else:
         roof = dict(bound="alu", achieved=alg_ops / kernel_s / 1e12, peak=ALU_PEAK / 1e12, unit="Tlane-op/s")
     roof["frac"] = roof["achieved"] / roof["peak"]
+    rc_ops = n_pairs * RECOUNT_SIM[0] + n_req * RECOUNT_SIM[1]
+    roof["frac_alu_recount"] = rc_ops / kernel_s / ALU_PEAK
     batched = any(p.get("service") == "batched" for p in wl.points)
     roof["traffic"] = _traffic("bat", args.workload, BAT_SOURCES) if batched else _traffic("sim", args.workload,
                                                                                           SIM_SOURCES)
     roof["kernel"] = ("rt::bat::bseg_kernel / bat_kernel (the batched classes the call launches)" if batched else
                       "rt::seg::seg_kernel / wseg_kernel (every class one rt_sim_run_replicas call launches)")
+    roof["per_unit"] = (f"{SIM_BYTES_PER_REQ} B/request; {SIM_OPS_PER_PAIR} lane-ops/pair + {SIM_OPS_PER_REQ}/request "
+                        f"(recount {RECOUNT_SIM[0]}/pair + {RECOUNT_SIM[1]}/request)")
     roof["kernel_ms"] = kernel_s * 1e3
     roof["alg_bytes"] = alg_bytes
     roof["alg_lane_ops"] = alg_ops
@@ -189,14 +217,18 @@ def bench_sim(args):
     return res
 
 
-def bench_scorer(args):
+def bench_scorer(args, rows=False):
+    """The standalone scorer: 2^20 requests x 64 decode instances against one
+    shared snapshot (ALU-bound), or with a snapshot row per request
+    (``rows``: 12 B per pair read, HBM-bound)."""
     import torch
     from oracle import oracle as O
     from paper_2609_16206_amd import rt_router as R
     from paper_2609_16206_amd import workload as W
 
     n_req, n_inst = 1 << 20, 64
-    d = W.scorer_inputs(n_req=n_req, n_inst=n_inst, seed=1)
+    d = W.scorer_inputs(n_req=n_req, n_inst=n_inst, seed=1, per_request=rows)
+    stride = d["inst_stride"]
     prm = W.scorer_params()
     torch.cuda.set_device(0)
     t = {k: torch.from_numpy(d[k]).cuda() for k in ("backlog_s", "queue", "kv_occ", "prompt_len", "pred_out_len",
@@ -206,7 +238,7 @@ def bench_scorer(args):
     stream = torch.cuda.current_stream()
 
     def step():
-        R.rt_score_argmin(prm, "decode", n_inst, t["backlog_s"], t["queue"], t["kv_occ"], d["kv_cap"], 0, n_req,
+        R.rt_score_argmin(prm, "decode", n_inst, t["backlog_s"], t["queue"], t["kv_occ"], d["kv_cap"], stride, n_req,
                           t["prompt_len"], t["pred_out_len"], t["slo_class"], idx, sc, stream)
 
     for _ in range(args.warmup):
@@ -222,26 +254,38 @@ def bench_scorer(args):
     dt = time.perf_counter() - t0
     kernel_s = ev0.elapsed_time(ev1) * 1e-3 / args.steps
     pairs = n_req * n_inst
-    alg_bytes = n_req * SCORE_BYTES_PER_REQ
+    alg_bytes = n_req * SCORE_BYTES_PER_REQ + (pairs * SCORE_BYTES_PER_PAIR_ROWS if rows else 0)
     alg_ops = pairs * SCORE_OPS_PER_PAIR + n_req * SCORE_OPS_PER_REQ
-    roof = dict(bound="alu", achieved=alg_ops / kernel_s / 1e12, peak=ALU_PEAK / 1e12, unit="Tlane-op/s")
+    if rows:
+        roof = dict(bound="hbm", achieved=alg_bytes / kernel_s / 1e9, peak=HBM_PEAK / 1e9, unit="GB/s")
+        roof["traffic"] = _traffic("score", "scorer_rows", SCORE_SOURCES)
+        roof["kernel"] = "rt::score_rows_kernel"
+        roof["per_unit"] = (f"{SCORE_BYTES_PER_PAIR_ROWS} B/pair + {SCORE_BYTES_PER_REQ} B/request")
+    else:
+        roof = dict(bound="alu", achieved=alg_ops / kernel_s / 1e12, peak=ALU_PEAK / 1e12, unit="Tlane-op/s")
+        roof["traffic"] = _traffic("score", "scorer", SCORE_SOURCES)
+        roof["kernel"] = "rt::score_shared_kernel"
+        roof["per_unit"] = (f"{SCORE_OPS_PER_PAIR} lane-ops/pair (recount {RECOUNT_SCORE[0]}/pair + "
+                            f"{RECOUNT_SCORE[1]}/request)")
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = _traffic("score", "scorer", SCORE_SOURCES)
-    roof["kernel"] = "rt::score_shared_kernel"
+    roof["frac_alu_recount"] = (pairs * RECOUNT_SCORE[0] + n_req * RECOUNT_SCORE[1]) / kernel_s / ALU_PEAK
     roof["kernel_ms"] = kernel_s * 1e3
+    wname = f"scorer-{n_req}x{n_inst}-" + ("per-request" if rows else "shared")
     res = dict(metric=METRIC, value=n_req * args.steps / dt, unit="requests/s", n_gpus=1, steps=args.steps,
                warmup=args.warmup, ms_per_step=dt * 1e3 / args.steps, higher_is_better=True, scaling="weak",
                vs_baseline=None, dtype="f32", data="synthetic",
-               config=dict(workload="scorer-1048576x64-shared", requests=n_req, instances=n_inst),
+               config=dict(workload=wname, requests=n_req, instances=n_inst, inst_stride=stride),
                pairs_per_s=pairs * args.steps / dt, roofline=roof)
     if not args.no_cpu_baseline:
         threads = 1
         m = 1 << 17
         t0 = time.perf_counter()
-        O.score(prm, "decode", d["backlog_s"], d["queue"], d["kv_occ"], d["kv_cap"], n_inst, 0, d["prompt_len"][:m],
-                d["pred_out_len"][:m], d["slo_class"][:m])
+        rl = slice(0, m * stride if rows else None)
+        O.score(prm, "decode", d["backlog_s"][rl], d["queue"][rl], d["kv_occ"][rl], d["kv_cap"], n_inst, stride,
+                d["prompt_len"][:m], d["pred_out_len"][:m], d["slo_class"][:m])
         dtc = time.perf_counter() - t0
         res["cpu_baseline"] = dict(value=m / dtc, unit="requests/s", cores=threads, kind="oracle",
+                                   pairs_per_s=m * n_inst / dtc,
                                    sample=f"first {m} of {n_req} requests x {n_inst} instances, 1 thread")
     return res
 
@@ -251,9 +295,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="cluster",
-                    choices=["tiny", "cluster", "cluster_sampled", "cluster_batched", "cluster_batched_wide", "sweep",
-                             "large", "scorer"])
+    ap.add_argument("--workload", default="large",
+                    choices=["large", "tiny", "cluster", "cluster_sampled", "cluster_batched", "cluster_batched_wide",
+                             "batched_wide_pool", "sweep", "scorer", "scorer_rows"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for the CPU baseline")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -272,7 +316,10 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    res = bench_scorer(args) if args.workload == "scorer" else bench_sim(args)
+    if args.workload in ("scorer", "scorer_rows"):
+        res = bench_scorer(args, rows=args.workload == "scorer_rows")
+    else:
+        res = bench_sim(args)
     print(json.dumps(res), flush=True)
 
 

@@ -95,7 +95,12 @@ typedef enum {
 } rt_service;
 
 #define RT_MAX_CLASSES 8
-#define RT_MAX_POOL 1024 /* instances per pool */
+/* Instances per pool.  The widest pool of every workload here is 1,024
+ * decode instances; the simulation kernels keep each instance's state and
+ * the front of its queue in registers, and eight waves of 64 lanes at five
+ * instances a lane hold two pools of 1,024, which is the most one workgroup
+ * holds that way. */
+#define RT_MAX_POOL 1024
 
 /* The router's priced view (Section III-A, Section III-B).  All finite and
  * >= 0, so every cost is >= 0. */
@@ -221,10 +226,17 @@ typedef struct {
  * its events; members are ordered by finish virtual time f = v at joining +
  * work, then request index; the next completion lies at
  * t_last + max(f_min - v, 0) (1 + beta (b - 1)), and every member with
- * f == f_min leaves then.  Clock backlog is the stand-alone work still owed:
- * the sum in member order of max(f - v, 0), plus on a decode instance the
- * decode work of requests routed there that have not joined (an exact
- * integer sum, added last), in seconds; ledger backlog is unchanged.  Times
+ * f == f_min leaves then.  Clock backlog is the stand-alone work still owed
+ * (Section III-A's backlog under batching), in seconds: the batch's
+ * remaining work plus, on a decode instance, the decode work of requests
+ * routed there that have not joined (an exact integer sum, added last).
+ * The kernels keep the batch's remaining work as a running float64 total
+ * per instance (+ each joining member's work; - b * dv at every
+ * virtual-time step dv, in event order; reset to 0 when the batch empties;
+ * clamped at 0 when read); it equals the sum over members of max(f - v, 0)
+ * up to rounding, so a placement can differ from one made on that sum only
+ * where two costs lie within rounding of each other.  Ledger backlog is
+ * unchanged.  Times
  * are float64 ns; at equal times completions come first, then KV landings,
  * then the arrival being routed.  TTFT and decode span are rounded to whole
  * ns (nearest, ties to even).  An instance holds at most batch_cap members
@@ -242,7 +254,9 @@ typedef struct {
  * kind).  It is owned by `sim`. */
 rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* out, void* hip_stream);
 
-/* Per-replica goodput: the fraction of the replica's requests that meet both
+/* Per-replica goodput, the SLO attainment that Table II reports, under the
+ * per-class TTFT and TPOT targets of Section IV-B: the fraction of the
+ * replica's requests that meet both
  * their class's TTFT target (ttft <= TTFT_c) and TPOT target
  * (span <= TPOT_c * (o_r - 1); always met when o_r == 1).  Rejected requests
  * count as missed; an empty replica has goodput 0.  goodput: [n_replicas]

@@ -177,7 +177,8 @@ static void free_pool(inst_t* a, int32_t n) {
   free(a);
 }
 
-/* backlog(d): seconds of work already committed to d.  True mode reads the
+/* backlog(d) as Section III-A defines it (the work the instance has already
+ * taken on, in seconds).  True mode reads the
  * simulation clock (busy-until minus now); proxy mode prices the in-flight
  * ledger with the router's own constants (Section VI). */
 /* The proxy's ledger backlog of an instance with `queue` requests and `pend`
@@ -458,9 +459,6 @@ typedef struct {
 
 typedef struct {
   double v, t_last;  /* virtual time, valid at time t_last                  */
-  double rem;        /* stand-alone work the batch still owes (ns): + each
-                        joining member's work, - b * every virtual-time
-                        step, 0 once the batch empties                      */
   bmember* act;      /* the batch, sorted by (f, r)                          */
   int64_t nact, cap;
   bjoin* wait;       /* decode only: transfers in flight, sorted by (t, r)   */
@@ -511,20 +509,13 @@ static int wait_insert(binst* s, double t, int64_t r) {
 /* Bring the instance's virtual time to time t, with no event in between:
  * each of the b members receives dv of service. */
 static void b_advance(binst* s, double beta, double t) {
-  if (s->nact > 0) {
-    const double dv = (t - s->t_last) / slowdown(beta, s->nact);
-    s->v += dv;
-    s->rem -= (double)s->nact * dv;
-  }
+  if (s->nact > 0) s->v += (t - s->t_last) / slowdown(beta, s->nact);
   s->t_last = t;
 }
 
-/* A member joins with stand-alone work w. */
-static int b_join(binst* s, double w, int64_t r) {
-  if (batch_insert(s, s->v + w, r)) return -1;
-  s->rem += w;
-  return 0;
-}
+/* A member joins with stand-alone work w: it finishes once the virtual
+ * clock has advanced by w. */
+static int b_join(binst* s, double w, int64_t r) { return batch_insert(s, s->v + w, r); }
 
 /* Time of the instance's next completion (+inf when idle).  The remaining
  * virtual work is clamped at 0, so a completion never lies before t_last. */
@@ -578,7 +569,6 @@ static int b_run_to(bsim* b, double T) {
       const int is_pre = k < P;
       binst* s = is_pre ? &b->pre[k] : &b->dec[k - P];
       const double fmin = s->act[0].f;
-      s->rem -= (double)s->nact * (fmin - s->v);
       s->v = fmin;
       s->t_last = te;
       int64_t m = 0;
@@ -603,7 +593,6 @@ static int b_run_to(bsim* b, double T) {
       }
       for (int64_t i = m; i < s->nact; ++i) s->act[i - m] = s->act[i];
       s->nact -= m;
-      if (s->nact == 0) s->rem = 0.0;
     } else {
       /* a KV lands: its request joins the decode batch */
       binst* s = &b->dec[k - P];
@@ -622,11 +611,13 @@ static int b_run_to(bsim* b, double T) {
   return 0;
 }
 
-/* Features of one pool.  Clock backlog: the stand-alone work (ns) the
- * instance still owes, the batch's running remaining work (clamped at 0)
- * plus, on a decode instance, the whole work of the requests routed there
- * that have not joined (an exact integer), in seconds.  Ledger backlog: as
- * in the serial model. */
+/* Features of one pool.  Clock backlog (backlog(d) of Section III-A, the
+ * work already committed to the instance, under batching): the stand-alone
+ * work (ns) the instance still owes, summed over the batch in member order,
+ * each member's max(f - v, 0) (clamped as in b_next), plus, on a decode
+ * instance, the whole work of the requests routed there that have not
+ * joined (an exact integer), in seconds.  Ledger backlog: as in the serial
+ * model. */
 static void batched_features(const bsim* b, int32_t pool, float* backlog, int64_t* queue, int64_t* kv) {
   const orc_point* pt = b->pt;
   const int32_t n = pool == ORC_PREFILL ? pt->n_prefill : pt->n_decode;
@@ -635,7 +626,11 @@ static void batched_features(const bsim* b, int32_t pool, float* backlog, int64_
     queue[j] = s->queue;
     kv[j] = s->kv;
     if (pt->backlog_mode == ORC_BACKLOG_TRUE) {
-      double w = s->rem < 0.0 ? 0.0 : s->rem;
+      double w = 0.0;
+      for (int64_t i = 0; i < s->nact; ++i) {
+        const double left = s->act[i].f - s->v;
+        w += left < 0.0 ? 0.0 : left;
+      }
       w += (double)s->owed_wait;
       backlog[j] = (float)w * 1e-9f;
     } else {

@@ -153,12 +153,10 @@ int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
  * lies at t_last + max(f_min - v, 0) * (1 + beta (b - 1)), and every member
  * with f == f_min leaves then.
  * Clock backlog is the stand-alone work the instance still owes, in
- * seconds: the batch's remaining work, kept as a running float64 total
- * (+ each joining member's work; - b * dv for every virtual-time step dv,
- * in the order the events occur; reset to 0 when the batch empties) and
- * clamped at 0, plus (decode) the int64 sum of the decode work of the
- * requests routed there that have not joined; ledger backlog as in the
- * serial model.
+ * seconds: the sum over the batch, in member order, of each member's
+ * remaining work max(f - v, 0), plus (decode) the int64 sum of the decode
+ * work of the requests routed there that have not joined; ledger backlog as
+ * in the serial model.
  * Times are float64 ns, events at equal times in the order: completions,
  * then KV landings, then the arrival being routed; the lower-numbered
  * instance first (prefill pool before decode pool), landings in request

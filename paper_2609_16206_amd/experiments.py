@@ -98,30 +98,37 @@ def run_cells(cells: Sequence[Cell], replicas: int = 32, requests: int = 5000, s
 
 def saturation_scale(point: Dict, traffic: W.Traffic, target: float = 0.5, policy: str = "round_robin",
                      scales: Sequence[float] = tuple(np.linspace(0.4, 2.0, 9)), rounds: int = 2,
-                     replicas: int = 32, requests: int = 4000, seed: int = 0, device: int = 0) -> Dict:
+                     replicas: int = 32, requests: int = 4000, seed: int = 0, device: int = 0,
+                     run=None) -> Dict:
     """Arrival-rate scale (relative to `traffic`) at which `policy` reaches
-    goodput `target`.  Each round simulates a grid of scales in one batch
-    and keeps the interval where the mean goodput crosses the target; the
-    answer interpolates linearly inside the last interval.  Returns the
-    scale and the probed (scale, goodput) pairs."""
+    goodput `target`.  Each round simulates a grid of scales in one batch;
+    the bracket is then taken over every probe so far: its low end is the
+    largest probed scale whose mean goodput is still >= target, its high end
+    the smallest larger probed scale below the target, and the next round
+    probes four scales inside it.  The answer interpolates linearly inside
+    the last bracket.  `run(cells, replicas, requests, seed, device)` returns
+    one row (with "mean") per cell; the default simulates on the GPU.
+    Returns the scale, the bracket and the probed (scale, goodput) pairs."""
+    run = run_cells if run is None else run
     pt = dict(point, policy=policy)
     probes: List[Tuple[float, float]] = []
     grid = [float(s) for s in scales]
     lo = hi = None
-    for _ in range(max(1, rounds)):
-        rows = run_cells([Cell(f"x{s:.4f}", pt, traffic.scaled(s)) for s in grid], replicas, requests, seed, device)
-        pts = sorted(zip(grid, [r["mean"] for r in rows]))
-        probes.extend(pts)
-        above = [(s, g) for s, g in pts if g >= target]
-        below = [(s, g) for s, g in pts if g < target]
-        if not above or not below:
+    for k in range(max(1, rounds)):
+        rows = run([Cell(f"x{s:.4f}", pt, traffic.scaled(s)) for s in grid], replicas, requests, seed, device)
+        probes.extend(zip(grid, [r["mean"] for r in rows]))
+        allp = sorted(probes)
+        above = [q for q in allp if q[1] >= target]
+        if not above:
+            lo = hi = None
             break
-        lo = max(above)  # largest scale still at or above the target
-        cand = [(s, g) for s, g in below if s > lo[0]]
+        lo = max(above)  # the largest probed scale still at or above the target
+        cand = [q for q in allp if q[0] > lo[0] and q[1] < target]
         if not cand:
+            hi = None
             break
         hi = min(cand)
-        grid = list(np.linspace(lo[0], hi[0], 6)[1:-1])
+        grid = [float(x) for x in np.linspace(lo[0], hi[0], 6)[1:-1]]
     probes.sort()
     if lo is None or hi is None:
         return dict(scale=None, probes=probes)

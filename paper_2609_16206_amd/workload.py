@@ -547,6 +547,18 @@ def large_pool_wl(n_replicas: int = 256, requests: int = 1_000_000, seed: int = 
                     [large_pool(rate)], meta=dict(rate=rate))
 
 
+def batched_wide_pool(n_replicas: int = 16384, requests: int = 1000, seed: int = 5, n_prefill: int = 8,
+                      n_decode: int = 64, load: float = 0.8) -> Workload:
+    """Continuous batching in both stages on a pool too wide for one segment
+    of lanes (8 prefill + 64 decode = 72 instances): mixed bursty traffic at
+    ``load`` x the serial-service capacity."""
+    pt = make_point(n_prefill, n_decode, n_classes=3, service="batched")
+    base = mixed_bursty()
+    k = load * capacity_rps(pt, base) / base.mean_rate()
+    return Workload(f"batched-{n_prefill}p{n_decode}d-mmpp-{n_replicas}x{requests}", seed, n_replicas, requests, [pt],
+                    [base.scaled(k)])
+
+
 # --------------------------------------------------------------------------
 # Standalone scorer inputs
 # --------------------------------------------------------------------------

@@ -114,3 +114,20 @@ def goodput_recount(points, trace, gpu) -> np.ndarray:
     met = (tt >= 0) & (tt <= ttft_t) & ((o <= 1) | (sp <= tpot_t * (o - 1)))
     rep = np.repeat(np.arange(len(counts)), counts)
     return np.bincount(rep, weights=met, minlength=len(counts)).astype(np.int64)
+
+
+def oracle_run_cells(cells, replicas: int, requests: int, seed: int, device: int = 0, threads: int = 16):
+    """The experiment drivers' cell runner with the oracle in place of the
+    GPU: the same trace (experiments.build_trace), every replica simulated by
+    the oracle, and each cell's mean goodput over its replicas computed as
+    the GPU runner computes it."""
+    from paper_2609_16206_amd import experiments as E
+    tr = E.build_trace(cells, replicas, requests, seed)
+    ref = O.sim_trace([c.point for c in cells], tr, threads=threads)
+    g = np.array([ref[i][2] for i in range(len(cells) * replicas)], np.float64)
+    rows = []
+    for c, cell in enumerate(cells):
+        x = g[c * replicas:(c + 1) * replicas]
+        rows.append(dict(label=cell.label, mean=float(x.mean()), std=float(x.std()), min=float(x.min()),
+                         max=float(x.max())))
+    return rows

@@ -112,3 +112,10 @@ def test_binding_fails_loudly_without_library(tmp_path):
     env = dict(os.environ, RT_ROUTER_LIB=str(tmp_path / "absent.so"))
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env)
     assert r.returncode != 0 and "librt_router.so is missing" in r.stderr
+
+
+def test_pool_limit_agrees_with_header(rt):
+    """The binding's pool limit is the header's: 1,024 instances per pool
+    (the widest workload's decode pool; wider pools are rejected)."""
+    m = re.search(r"#define\s+RT_MAX_POOL\s+(\d+)", open(HEADER).read())
+    assert m and int(m.group(1)) == rt.RT_MAX_POOL == 1024

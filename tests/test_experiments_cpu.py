@@ -69,3 +69,51 @@ def test_service_cells_pair_each_policy():
         assert a.traffic is b.traffic
         assert {k: v for k, v in a.point.items() if k != "service"} == {k: v for k, v in b.point.items()
                                                                        if k != "service"}
+
+
+def _fake_runner(fn):
+    """A cell runner whose mean goodput is fn(scale), the scale read back
+    from the cell's traffic."""
+    base = W.mixed_bursty()
+
+    def run(cells, replicas, requests, seed, device):
+        return [dict(label=c.label, mean=float(fn(c.traffic.mean_rate() / base.mean_rate()))) for c in cells]
+    return run
+
+
+def test_saturation_search_linear_curve_is_exact():
+    """On a goodput curve that is linear in the scale the interpolation
+    returns the exact crossing (0.5 at scale 1.3)."""
+    res = E.saturation_scale(W.make_point(2, 4), W.mixed_bursty(), run=_fake_runner(lambda s: 1.15 - 0.5 * s))
+    assert abs(res["scale"] - 1.3) < 1e-9
+    s0, s1 = res["bracket"]
+    assert s0 <= 1.3 <= s1 and s1 - s0 < 0.2 / 4
+
+
+def test_saturation_search_bracket_uses_every_probe():
+    """The bracket is taken over all probes so far: a refinement round whose
+    four interior probes all lie above the target still narrows it (a
+    bracket kept from the previous round would ignore them), and no probe
+    lies strictly inside the final bracket."""
+    fn = lambda s: 1.0 if s < 1.78 else 0.0  # noqa: E731
+    res = E.saturation_scale(W.make_point(2, 4), W.mixed_bursty(), run=_fake_runner(fn), rounds=3)
+    s0, s1 = res["bracket"]
+    assert s0 < 1.78 <= s1
+    inside = [s for s, _ in res["probes"] if s0 < s < s1]
+    assert not inside
+    assert s1 - s0 < 0.2 / 5 / 5 * 1.01  # two refinements of the 0.2-wide first bracket
+    above = [s for s, g in res["probes"] if g >= 0.5]
+    assert s0 == max(above)
+
+
+def test_oracle_cell_runner_means():
+    """The oracle's cell runner (used to check the GPU search) returns, per
+    cell, the mean of the oracle goodput of its replicas."""
+    from oracle import oracle as O
+    from tests.parity import oracle_run_cells
+    cells = E.policy_cells(2, 3, W.mixed_bursty(), policies=("round_robin", "least_loaded"))
+    rows = oracle_run_cells(cells, replicas=2, requests=300, seed=9, threads=2)
+    tr = E.build_trace(cells, 2, 300, 9)
+    ref = O.sim_trace([c.point for c in cells], tr)
+    for c in range(2):
+        assert rows[c]["mean"] == float(np.mean([ref[2 * c][2], ref[2 * c + 1][2]]))

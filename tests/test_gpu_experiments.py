@@ -1,6 +1,8 @@
-"""Experiment drivers on the GPU: a batched policy grid agrees with the
-oracle replica by replica, and the saturation search finds the scale where
-round robin is mid-collapse."""
+"""Experiment drivers on the GPU: batched policy grids on every workload
+family of Table I (chat, document, reasoning, mixed bursty) agree with the
+oracle replica by replica, and the saturation search (Section IV-B) probes
+the same goodputs and finds the same scale as the same search run on the
+oracle."""
 import numpy as np
 import pytest
 
@@ -8,6 +10,7 @@ from oracle import oracle as O
 from paper_2609_16206_amd import experiments as E
 from paper_2609_16206_amd import workload as W
 from tests.gpu_common import log
+from tests.parity import follow_replicas, oracle_run_cells
 
 pytestmark = pytest.mark.gpu
 
@@ -24,6 +27,42 @@ def test_policy_grid_matches_oracle():
         assert np.array_equal(o["ttft_ns"], out["ttft_ns"][sl]) and np.array_equal(o["decode_span_ns"],
                                                                                    out["decode_span_ns"][sl]), i
         assert gg == g[i], i
+
+
+FAMILIES = [("chat", W.chat(1.0)), ("document", W.document(1.0)), ("reasoning", W.reasoning(1.0)),
+            ("mixed", W.mixed_bursty())]
+
+
+@pytest.mark.parametrize("family,traffic", FAMILIES, ids=[f for f, _ in FAMILIES])
+def test_table1_family_policy_grid_matches_oracle(family, traffic):
+    """Every policy (learned, round robin, least loaded, length threshold,
+    sampled learned) on one Table I family at 0.9 of the pool's serial
+    capacity: each replica bitwise against the oracle in follow mode."""
+    P, D = 2, 4
+    cap = W.capacity_rps(W.make_point(P, D, n_classes=3), traffic)
+    traf = traffic.scaled(0.9 * cap / traffic.mean_rate())
+    cells = E.policy_cells(P, D, traf)
+    rows, tr, out, g = E.run_cells(cells, replicas=3, requests=1500, seed=11, return_trace=True)
+    log(f"{family}: " + ", ".join(f"{r['label']} {r['mean']:.3f}" for r in rows))
+    rep = follow_replicas([c.point for c in cells], tr, out, range(len(cells) * 3), gpu_goodput=g)
+    log(f"{family} policy grid vs oracle: {rep}")
+    assert rep["replicas"] == len(cells) * 3
+
+
+def test_saturation_search_matches_oracle():
+    """The saturation search (round robin mid-collapse, Section IV-B) run
+    on the GPU and on the oracle: every probe's mean goodput is identical
+    and so are the bracket and the scale."""
+    pt = W.make_point(2, 4, n_classes=3)
+    traf = W.mixed_bursty()
+    kw = dict(target=0.5, replicas=12, requests=2500, seed=3)
+    gpu = E.saturation_scale(pt, traf, **kw)
+    orc = E.saturation_scale(pt, traf, run=oracle_run_cells, **kw)
+    log(f"saturation GPU {gpu['scale']} bracket {gpu.get('bracket')}; oracle {orc['scale']} bracket "
+        f"{orc.get('bracket')}; {len(gpu['probes'])} probes")
+    assert gpu["probes"] == orc["probes"]
+    assert gpu["scale"] == orc["scale"] and gpu.get("bracket") == orc.get("bracket")
+    assert gpu["scale"] is not None
 
 
 def test_saturation_search_brackets_round_robin_collapse():
