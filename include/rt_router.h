@@ -254,6 +254,31 @@ typedef struct {
  * kind).  It is owned by `sim`. */
 rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* out, void* hip_stream);
 
+/* For callers that cannot allocate memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): the same
+ * simulation as rt_sim_run_replicas, with the same arguments and outputs,
+ * bit for bit, for serial-service points, calling no hipMalloc, hipFree or
+ * other allocating routine.  Its FIFO record planes and its work list live
+ * in a fixed 64 MiB device array that the library holds on every GPU it has
+ * run on until the process ends (its address is resolved once per device,
+ * by rt_sim_create), and its launch is planned in fixed host arrays.
+ * Limits, each returned as RT_ERANGE before anything is launched: at most
+ * 65,536 replicas per call and 4,096 points per simulator, and at most
+ * 64 MiB of scratch: 64 bytes per request of trace->n_requests (128 for
+ * points with the proxy backlog, 192 when a call holds both kinds), plus
+ * 4 bytes per replica, plus a fixed 192 KiB at most (dummy records ahead
+ * of the record planes).  A point with
+ * continuous-batching service returns RT_EUNSUPPORTED.  Every kernel class
+ * runs on `hip_stream` in turn (rt_sim_run_replicas runs them side by side
+ * on streams of its own).  Nothing in the array needs to start at zero:
+ * every record is written before it is read.  All calls on one GPU share
+ * the array, so calls that overlap on one GPU (on different streams, or
+ * from different threads without ordering) race and their outputs are not
+ * valid; calls on one stream are ordered.  The host-side planning arrays
+ * are shared by all threads and guarded by a lock: the call waits for the
+ * offsets read-back and for the work list's upload before it returns. */
+rt_status rt_sim_run_replicas_noalloc(rt_sim* sim, const rt_trace* trace, rt_sim_out* out, void* hip_stream);
+
 /* Per-replica goodput, the SLO attainment that Table II reports, under the
  * per-class TTFT and TPOT targets of Section IV-B: the fraction of the
  * replica's requests that meet both

@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -46,6 +47,15 @@ constexpr int64_t kMaxNs = int64_t(1) << 40;
 constexpr int32_t kMaxBatchCap = 65536;
 constexpr int32_t kDefaultBatchCap = 256;
 constexpr int kSimds = 256 * 4;  // MI355X: 256 compute units x 4 SIMDs
+
+// Limits of rt_sim_run_replicas_noalloc: the device scratch each GPU holds
+// for it (record planes and the work list), and the host-side planning
+// arrays, sized for this many replicas, points and kernel classes.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+constexpr int64_t kNoAllocMaxReplicas = 65536;
+constexpr int32_t kNoAllocMaxPoints = 4096;
+constexpr int kMaxClassSlots = 256;
+constexpr int kMaxDevices = 64;
 
 std::string check_point(const rt_point& p) {
   if (p.n_prefill < 1 || p.n_decode < 1) return "pool sizes must be >= 1";
@@ -165,6 +175,147 @@ double seg_step_cost(const rt::SimClass& c) {
 
 }  // namespace
 
+// The file-scope device scratch of rt_sim_run_replicas_noalloc (one copy per
+// GPU, held until the process ends).  Host code never passes this name to a
+// kernel: it resolves the array's address on each device once
+// (static_scratch) and passes that.
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+namespace {
+
+// The points of a simulator as the planner reads them: how many, and the
+// kernel classes that hold each.
+struct rt_sim_points {
+  size_t n;
+  const std::vector<int>* classes;
+};
+
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices];  // scratch's address on each device, once resolved
+
+// The address of `scratch` on `device` (current): resolved on the first
+// call for the device and kept.
+rt_status static_scratch(int device, void** out) {
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (device < 0 || device >= kMaxDevices) return fail(RT_ERANGE, "static scratch: device index beyond the table");
+  if (!g_scratch_dev[device]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!ptr) return fail(RT_EDEVICE, "hipGetSymbolAddress(scratch): null address");
+    g_scratch_dev[device] = ptr;
+  }
+  *out = g_scratch_dev[device];
+  return RT_OK;
+}
+
+// Storage of one launch plan, owned by the caller (growable vectors for
+// rt_sim_run_replicas, fixed static arrays for the no-alloc variant).
+struct PlanBufs {
+  int64_t* off;      // [n + 1] offsets, read back
+  int32_t* pp;       // [n] replica -> point, read back
+  int64_t* reps_of;  // [npts] non-empty replicas per point
+  int* choice;       // [npts] each point's kernel class
+  int* wider;        // [npts] working copy for the widening pass
+  int64_t* count;    // [ncls] replicas per class
+  int64_t* start;    // [ncls] first work-list slot per class
+  double* cost;      // [ncls] request-lanes per class (launch order)
+  int32_t* work;     // [n] replica ids, grouped by class
+  int* act;          // [ncls] classes with work, dearest first
+  int n_act;
+};
+
+// Plan.  Each point runs one kernel class.  With few replicas (fewer waves,
+// at the shortest-step classes, than twice the GPU's SIMDs) every replica is
+// a latency chain and takes the shortest-step class; with many, the GPU's
+// issue rate is the limit and each point takes the segment class with the
+// fewest issue slots per replica-step (lanes x step cost).  Then replicas
+// are grouped by class, longest first so that long chains start early (equal
+// lengths in replica order); empty replicas need no work.  Classes with work
+// are listed dearest first.  Allocates nothing.
+void plan_launch(const rt_sim_points& sp, int64_t n, PlanBufs& b) {
+  const int ncls = rt::sim_class_count();
+  const size_t npts = sp.n;
+  for (size_t k = 0; k < npts; ++k) b.reps_of[k] = 0;
+  for (int64_t i = 0; i < n; ++i)
+    if (b.off[i + 1] > b.off[i]) b.reps_of[b.pp[i]] += 1;
+  double waves = 0.0;
+  for (size_t k = 0; k < npts; ++k) waves += (double)b.reps_of[k] * rt::sim_class(sp.classes[k][0]).S / 64.0;
+  const bool many = waves >= 2.0 * kSimds;
+  for (size_t k = 0; k < npts; ++k) {
+    const std::vector<int>& fit = sp.classes[k];
+    b.choice[k] = fit[0];
+    if (!many) continue;
+    double best = -1.0;
+    for (int c : fit) {
+      const rt::SimClass sc = rt::sim_class(c);
+      if (sc.kind != rt::kSeg) continue;
+      const double cost = sc.S * seg_step_cost(sc);
+      if (best < 0.0 || cost < best) {
+        best = cost;
+        b.choice[k] = c;
+      }
+    }
+  }
+  // With fewer waves than SIMDs, spread the replicas out: doubling the
+  // segment width of every one-instance-per-lane class (the extra lanes
+  // idle) halves the replicas in each wave, and a wave's step costs as much
+  // as its slowest replica's step.  Widen while the waves keep growing and
+  // still fit one per SIMD.
+  if (!many) {
+    for (;;) {
+      double w2 = 0.0, w1 = 0.0;
+      for (size_t k = 0; k < npts; ++k) {
+        b.wider[k] = b.choice[k];
+        if (b.reps_of[k] == 0) continue;
+        const rt::SimClass sc = rt::sim_class(b.choice[k]);
+        w1 += std::ceil((double)b.reps_of[k] * sc.S / 64.0);
+        if ((sc.kind == rt::kSeg || sc.kind == rt::kBat) && sc.MP == 1 && sc.S < 64)
+          for (int c : sp.classes[k]) {
+            const rt::SimClass wc = rt::sim_class(c);
+            if (wc.kind == sc.kind && wc.mode == sc.mode && wc.MP == 1 && wc.S == 2 * sc.S) b.wider[k] = c;
+          }
+        w2 += std::ceil((double)b.reps_of[k] * rt::sim_class(b.wider[k]).S / 64.0);
+      }
+      if (!(w2 > w1 && w2 <= kSimds)) break;
+      for (size_t k = 0; k < npts; ++k) b.choice[k] = b.wider[k];
+    }
+  }
+  // group by class (counting sort, replica order kept), then longest first
+  for (int c = 0; c < ncls; ++c) b.count[c] = 0;
+  for (int64_t i = 0; i < n; ++i)
+    if (b.off[i + 1] > b.off[i]) b.count[b.choice[b.pp[i]]] += 1;
+  int64_t pos = 0;
+  for (int c = 0; c < ncls; ++c) {
+    b.start[c] = pos;
+    pos += b.count[c];
+  }
+  for (int c = 0; c < ncls; ++c) b.cost[c] = 0.0;
+  {
+    // (start[] is used as a fill cursor, then restored)
+    for (int64_t i = 0; i < n; ++i)
+      if (b.off[i + 1] > b.off[i]) {
+        const int c = b.choice[b.pp[i]];
+        b.work[b.start[c]++] = (int32_t)i;
+        b.cost[c] += (double)(b.off[i + 1] - b.off[i]) * rt::sim_class(c).S;
+      }
+    for (int c = 0; c < ncls; ++c) b.start[c] -= b.count[c];
+  }
+  const int64_t* off = b.off;
+  for (int c = 0; c < ncls; ++c)
+    std::sort(b.work + b.start[c], b.work + b.start[c] + b.count[c], [off](int32_t x, int32_t y) {
+      const int64_t lx = off[x + 1] - off[x], ly = off[y + 1] - off[y];
+      return lx != ly ? lx > ly : x < y;
+    });
+  b.n_act = 0;
+  for (int c = 0; c < ncls; ++c)
+    if (b.count[c] > 0) b.act[b.n_act++] = c;
+  const double* cost = b.cost;
+  std::sort(b.act, b.act + b.n_act, [cost](int x, int y) { return cost[x] != cost[y] ? cost[x] > cost[y] : x < y; });
+}
+
+}  // namespace
+
 struct rt_sim {
   int device = 0;
   std::vector<rt_point> points;
@@ -178,6 +329,7 @@ struct rt_sim {
   int32_t* d_work = nullptr;
   size_t work_cap = 0;
   int32_t* h_work = nullptr;  // pinned staging for the work list
+  void* static_scratch = nullptr;  // this device's copy of `scratch` (no-alloc entry point)
   size_t h_work_cap = 0;
   hipEvent_t upload_done = nullptr;
   bool upload_pending = false;
@@ -250,6 +402,8 @@ rt_status rt_sim_create(const rt_point* points, int32_t n_points, int32_t device
     st = hip_fail(e, "hipMemset(flag)");
   } else if ((e = hipEventCreateWithFlags(&s->upload_done, hipEventDisableTiming)) != hipSuccess) {
     st = hip_fail(e, "hipEventCreate");
+  } else if ((st = static_scratch(device, &s->static_scratch)) != RT_OK) {
+    // (message set by static_scratch)
   } else if ((e = hipDeviceSynchronize()) != hipSuccess) {
     st = hip_fail(e, "hipDeviceSynchronize");
   }
@@ -293,6 +447,22 @@ static rt_status check_trace(const rt_sim* sim, const rt_trace* tr, const rt_sim
   return RT_OK;
 }
 
+// Validates offsets and the replica->point map as read back to the host.
+static rt_status check_plan_inputs(const rt_sim* sim, const rt_trace* tr, const int64_t* off, const int32_t* pp,
+                                   const char* fn) {
+  const int64_t n = tr->n_replicas;
+  if (off[0] < 0) return fail(RT_EINVAL, std::string(fn) + ": offsets[0] < 0");
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t len = off[i + 1] - off[i];
+    if (len < 0) return fail(RT_EINVAL, std::string(fn) + ": offsets decrease at replica " + std::to_string(i));
+    if (len > INT32_MAX) return fail(RT_ERANGE, std::string(fn) + ": replica " + std::to_string(i) + " has >= 2^31 requests");
+    if (pp[i] < 0 || pp[i] >= (int32_t)sim->points.size())
+      return fail(RT_EINVAL, std::string(fn) + ": param_point out of range at replica " + std::to_string(i));
+  }
+  if (off[n] > tr->n_requests) return fail(RT_EINVAL, std::string(fn) + ": offsets[n_replicas] > n_requests");
+  return RT_OK;
+}
+
 // Reads offsets and the replica->point map back to the host and validates them.
 static rt_status read_plan_inputs(const rt_sim* sim, const rt_trace* tr, hipStream_t stream,
                                   std::vector<int64_t>& off, std::vector<int32_t>& pp, const char* fn) {
@@ -304,15 +474,88 @@ static rt_status read_plan_inputs(const rt_sim* sim, const rt_trace* tr, hipStre
     e = hipMemcpyAsync(pp.data(), tr->param_point, sizeof(int32_t) * n, hipMemcpyDeviceToHost, stream);
   if (e == hipSuccess) e = hipStreamSynchronize(stream);
   if (e != hipSuccess) return hip_fail(e, "reading offsets/param_point");
-  if (off[0] < 0) return fail(RT_EINVAL, std::string(fn) + ": offsets[0] < 0");
-  for (int64_t i = 0; i < n; ++i) {
-    const int64_t len = off[i + 1] - off[i];
-    if (len < 0) return fail(RT_EINVAL, std::string(fn) + ": offsets decrease at replica " + std::to_string(i));
-    if (len > INT32_MAX) return fail(RT_ERANGE, std::string(fn) + ": replica " + std::to_string(i) + " has >= 2^31 requests");
-    if (pp[i] < 0 || pp[i] >= (int32_t)sim->points.size())
-      return fail(RT_EINVAL, std::string(fn) + ": param_point out of range at replica " + std::to_string(i));
+  return check_plan_inputs(sim, tr, off.data(), pp.data(), fn);
+}
+
+// Byte size of the serial classes' record planes for n_requests requests:
+// for each record size in use (32 bytes, or 64 for the classes that price the
+// ledger) a plane per pool, each its dummy records followed by one record per
+// request, 256-byte aligned.  Classes of one call run side by side, so each
+// size has planes of its own.
+struct RecLayout {
+  bool any_serial = false, any_ledger = false, any_plain = false;
+  size_t plain_plane = 0, ledger_plane = 0, bytes = 0;
+};
+
+static RecLayout rec_layout(const PlanBufs& b, size_t nreq) {
+  RecLayout L;
+  for (int k = 0; k < b.n_act; ++k) {
+    const rt::SimClass c = rt::sim_class(b.act[k]);
+    if (c.kind == rt::kBat) continue;
+    L.any_serial = true;
+    (rt::mode_ledger(c.mode) ? L.any_ledger : L.any_plain) = true;
   }
-  if (off[n] > tr->n_requests) return fail(RT_EINVAL, std::string(fn) + ": offsets[n_replicas] > n_requests");
+  static_assert(((size_t)rt::kDummyRecords << rt::rec_shift(false)) % 256 == 0, "planes start 256-byte aligned");
+  auto plane_bytes = [&](bool ledger) {
+    return (((nreq + rt::kDummyRecords) << rt::rec_shift(ledger)) + 255) / 256 * 256;
+  };
+  L.plain_plane = L.any_plain ? plane_bytes(false) : 0;
+  L.ledger_plane = L.any_ledger ? plane_bytes(true) : 0;
+  L.bytes = L.any_serial ? 2 * L.plain_plane + 2 * L.ledger_plane + 256 : 0;
+  return L;
+}
+
+// The kernels' arguments for a call, with the record planes carved from
+// `sc` (laid out as rec_layout says); rec[] is set per class at launch.
+static rt::SimArgs sim_args(const rt_sim* sim, const rt_trace* trace, const rt_sim_out* out, const RecLayout& L,
+                            char* sc, char* (&planes)[2][2]) {
+  rt::SimArgs a;
+  a.points = sim->d_points;
+  a.offsets = trace->offsets;
+  a.param_point = trace->param_point;
+  a.arrival = trace->arrival_ns;
+  a.plen = trace->prompt_len;
+  a.olen = trace->out_len;
+  a.ohat = trace->pred_out_len;
+  a.cls = trace->slo_class;
+  a.samp = trace->sample_bits;
+  a.i_pre = out->i_pre;
+  a.i_dec = out->i_dec;
+  a.ttft = out->ttft_ns;
+  a.span = out->decode_span_ns;
+  a.work = nullptr;
+  a.n_work = 0;
+  // record planes by record size: index 0 of each pool's plane
+  for (int k = 0; k < 2; ++k) planes[0][k] = planes[1][k] = nullptr;
+  for (int k = 0; k < 2 && sc && L.any_serial; ++k) {
+    if (L.any_plain) planes[0][k] = sc + k * L.plain_plane + ((size_t)rt::kDummyRecords << rt::rec_shift(false));
+    if (L.any_ledger)
+      planes[1][k] =
+          sc + 2 * L.plain_plane + k * L.ledger_plane + ((size_t)rt::kDummyRecords << rt::rec_shift(true));
+  }
+  a.rec[0] = a.rec[1] = nullptr;
+  a.flag = sim->d_flag;
+  return a;
+}
+
+// Launches class c of the plan over its replicas (work list at d_work).
+static hipError_t launch_class(int c, rt::SimArgs a, const PlanBufs& b, const int32_t* d_work, char* (&planes)[2][2],
+                               const rt::BatScratch* bs, hipStream_t where) {
+  a.work = d_work + b.start[c];
+  a.n_work = b.count[c];
+  const int lg = rt::mode_ledger(rt::sim_class(c).mode) ? 1 : 0;
+  a.rec[0] = planes[lg][0];
+  a.rec[1] = planes[lg][1];
+  return rt::sim_class(c).kind == rt::kBat ? rt::launch_bat(rt::sim_class(c), a, bs[c], where)
+                                           : rt::launch_sim(rt::sim_class(c), a, where);
+}
+
+// The sampled policy reads the trace's candidate words.
+static rt_status check_sample_bits(const rt_sim* sim, const rt_trace* trace, const PlanBufs& b, const char* fn) {
+  for (size_t k = 0; k < sim->points.size(); ++k)
+    if (b.reps_of[k] > 0 && sim->points[k].policy == RT_POLICY_LEARNED_SAMPLED && !trace->sample_bits)
+      return fail(RT_EINVAL, std::string(fn) + ": point " + std::to_string(k) +
+                                 " samples candidates but trace->sample_bits is NULL");
   return RT_OK;
 }
 
@@ -326,131 +569,59 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
   hipStream_t stream = (hipStream_t)hip_stream;
   std::vector<int64_t> off;
   std::vector<int32_t> pp;
-  if ((st = read_plan_inputs(sim, trace, stream, off, pp, "rt_sim_run_replicas")) != RT_OK) return st;
+  if ((st = read_plan_inputs(sim, trace, stream, off, pp, "rt_sim_run_replicas")) != RT_OK)
+    return st;
 
-  // Plan.  Each point runs one kernel class.  With few replicas (fewer
-  // waves, at the shortest-step classes, than twice the GPU's SIMDs) every
-  // replica is a latency chain and takes the shortest-step class; with many,
-  // the GPU's issue rate is the limit and each point takes the segment class
-  // with the fewest issue slots per replica-step (lanes x step cost).  Then
-  // replicas are bucketed by class, longest first so that long chains start
-  // early; empty replicas need no work.
   const int ncls = rt::sim_class_count();
   const int64_t n = trace->n_replicas;
   const size_t npts = sim->points.size();
-  std::vector<int64_t> reps_of(npts, 0);
-  for (int64_t i = 0; i < n; ++i)
-    if (off[i + 1] > off[i]) reps_of[pp[i]] += 1;
-  for (size_t k = 0; k < npts; ++k)
-    if (reps_of[k] > 0 && sim->points[k].policy == RT_POLICY_LEARNED_SAMPLED && !trace->sample_bits)
-      return fail(RT_EINVAL, "rt_sim_run_replicas: point " + std::to_string(k) +
-                                 " samples candidates but trace->sample_bits is NULL");
-  double waves = 0.0;
-  for (size_t k = 0; k < npts; ++k) waves += (double)reps_of[k] * rt::sim_class(sim->point_classes[k][0]).S / 64.0;
-  const bool many = waves >= 2.0 * kSimds;
-  std::vector<int> choice(npts);
-  for (size_t k = 0; k < npts; ++k) {
-    const std::vector<int>& fit = sim->point_classes[k];
-    choice[k] = fit[0];
-    if (!many) continue;
-    double best = -1.0;
-    for (int c : fit) {
-      const rt::SimClass sc = rt::sim_class(c);
-      if (sc.kind != rt::kSeg) continue;
-      const double cost = sc.S * seg_step_cost(sc);
-      if (best < 0.0 || cost < best) {
-        best = cost;
-        choice[k] = c;
-      }
-    }
-  }
-  // With fewer waves than SIMDs, spread the replicas out: doubling the
-  // segment width of every one-instance-per-lane class (the extra lanes
-  // idle) halves the replicas in each wave, and a wave's step costs as much
-  // as its slowest replica's step.  Widen while the waves keep growing and
-  // still fit one per SIMD.
-  if (!many) {
-    for (;;) {
-      std::vector<int> wider(choice);
-      double w2 = 0.0, w1 = 0.0;
-      for (size_t k = 0; k < npts; ++k) {
-        if (reps_of[k] == 0) continue;
-        const rt::SimClass sc = rt::sim_class(choice[k]);
-        w1 += std::ceil((double)reps_of[k] * sc.S / 64.0);
-        if ((sc.kind == rt::kSeg || sc.kind == rt::kBat) && sc.MP == 1 && sc.S < 64)
-          for (int c : sim->point_classes[k]) {
-            const rt::SimClass wc = rt::sim_class(c);
-            if (wc.kind == sc.kind && wc.mode == sc.mode && wc.MP == 1 && wc.S == 2 * sc.S) wider[k] = c;
-          }
-        w2 += std::ceil((double)reps_of[k] * rt::sim_class(wider[k]).S / 64.0);
-      }
-      if (!(w2 > w1 && w2 <= kSimds)) break;
-      choice.swap(wider);
-    }
-  }
-  std::vector<std::vector<int32_t>> buckets(ncls);
-  for (int64_t i = 0; i < n; ++i)
-    if (off[i + 1] > off[i]) buckets[choice[pp[i]]].push_back((int32_t)i);
-  for (auto& b : buckets)
-    std::stable_sort(b.begin(), b.end(), [&](int32_t x, int32_t y) {
-      return off[x + 1] - off[x] > off[y + 1] - off[y];
-    });
+  std::vector<int64_t> reps_of(npts), count(ncls), start(ncls);
+  std::vector<int> choice(npts), wider(npts), act(ncls);
+  std::vector<double> cost(ncls);
+  std::vector<int32_t> work_list(n);
+  PlanBufs b{off.data(), pp.data(), reps_of.data(), choice.data(), wider.data(), count.data(), start.data(),
+             cost.data(), work_list.data(), act.data(), 0};
+  plan_launch(rt_sim_points{npts, sim->point_classes.data()}, n, b);
+  if ((st = check_sample_bits(sim, trace, b, "rt_sim_run_replicas")) != RT_OK) return st;
 
   hipError_t e;
-  // Scratch of the serial classes: for each record size in use (32 bytes,
-  // or 64 for the classes that price the ledger) a plane per pool, each its
-  // dummy records followed by one record per request, 256-byte aligned.
-  // Classes of one call run side by side, so each size has planes of its own.
-  bool any_serial = false, any_ledger = false, any_plain = false;
-  std::vector<int> bat_classes;
-  for (int c = 0; c < ncls; ++c) {
-    if (buckets[c].empty()) continue;
-    if (rt::sim_class(c).kind == rt::kBat) {
-      bat_classes.push_back(c);
-    } else {
-      any_serial = true;
-      (rt::mode_ledger(rt::sim_class(c).mode) ? any_ledger : any_plain) = true;
-    }
-  }
   const size_t nreq = (size_t)trace->n_requests;
-  static_assert(((size_t)rt::kDummyRecords << rt::rec_shift(false)) % 256 == 0, "planes start 256-byte aligned");
-  auto plane_bytes = [&](bool ledger) {
-    return (((nreq + rt::kDummyRecords) << rt::rec_shift(ledger)) + 255) / 256 * 256;
-  };
-  const size_t plain_plane = any_plain ? plane_bytes(false) : 0, ledger_plane = any_ledger ? plane_bytes(true) : 0;
-  const size_t need = any_serial ? 2 * plain_plane + 2 * ledger_plane + 256 : 0;
-  if (need > sim->scratch_bytes) {
+  const RecLayout L = rec_layout(b, nreq);
+  if (L.bytes > sim->scratch_bytes) {
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
     if (sim->d_scratch) (void)hipFree(sim->d_scratch);
     sim->d_scratch = nullptr;
     sim->scratch_bytes = 0;
-    if ((e = hipMalloc(&sim->d_scratch, need)) != hipSuccess) return hip_fail(e, "hipMalloc(scratch)");
-    sim->scratch_bytes = need;
+    if ((e = hipMalloc(&sim->d_scratch, L.bytes)) != hipSuccess) return hip_fail(e, "hipMalloc(scratch)");
+    sim->scratch_bytes = L.bytes;
   }
   // Scratch of the batched classes: per-instance state and two rings per
   // instance for every lane of each, sized by the largest pool and capacity
   // among that class's replicas' points; one allocation, carved in turn.
   std::vector<rt::BatScratch> bs(ncls);
-  if (!bat_classes.empty()) {
+  {
     struct Dim {
+      int c;
       int64_t S;
       int32_t NI, C;
     };
     std::vector<Dim> dims;
     size_t bneed = 256;
-    for (int c : bat_classes) {
+    for (int k = 0; k < b.n_act; ++k) {
+      const int c = b.act[k];
+      const rt::SimClass sc = rt::sim_class(c);
+      if (sc.kind != rt::kBat) continue;
       int32_t NI = 1, C = 2;
-      for (int32_t r : buckets[c]) {
-        const rt_point& q = sim->points[pp[r]];
+      for (int64_t j = b.start[c]; j < b.start[c] + b.count[c]; ++j) {
+        const rt_point& q = sim->points[pp[work_list[j]]];
         NI = std::max(NI, q.n_prefill + q.n_decode);
         C = std::max(C, q.batch_cap == 0 ? kDefaultBatchCap : q.batch_cap);
       }
-      const rt::SimClass sc = rt::sim_class(c);
       if (sc.MP == 1) NI = 1;  // a segment class: one instance per lane
-      dims.push_back(Dim{rt::bat_lanes(sc, (int64_t)buckets[c].size()), NI, C});
+      dims.push_back(Dim{c, rt::bat_lanes(sc, b.count[c]), NI, C});
       bneed += rt::bat_scratch_bytes(dims.back().S, NI, C);
     }
-    if (bneed > sim->bscratch_bytes) {
+    if (!dims.empty() && bneed > sim->bscratch_bytes) {
       if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
       if (sim->d_bscratch) (void)hipFree(sim->d_bscratch);
       sim->d_bscratch = nullptr;
@@ -459,9 +630,9 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
       sim->bscratch_bytes = bneed;
     }
     size_t at = 0;
-    for (size_t k = 0; k < bat_classes.size(); ++k) {
-      bs[bat_classes[k]] = rt::bat_scratch_carve(sim->d_bscratch + at, dims[k].S, dims[k].NI, dims[k].C);
-      at += rt::bat_scratch_bytes(dims[k].S, dims[k].NI, dims[k].C);
+    for (const Dim& d : dims) {
+      bs[d.c] = rt::bat_scratch_carve(sim->d_bscratch + at, d.S, d.NI, d.C);
+      at += rt::bat_scratch_bytes(d.S, d.NI, d.C);
     }
   }
   if ((size_t)n > sim->work_cap) {
@@ -484,61 +655,28 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
       return hip_fail(e, "hipHostMalloc(work)");
     sim->h_work_cap = (size_t)n;
   }
-  size_t pos = 0;
-  std::vector<size_t> start(ncls);
-  for (int c = 0; c < ncls; ++c) {
-    start[c] = pos;
-    std::copy(buckets[c].begin(), buckets[c].end(), sim->h_work + pos);
-    pos += buckets[c].size();
-  }
-  if (pos > 0) {
-    if ((e = hipMemcpyAsync(sim->d_work, sim->h_work, sizeof(int32_t) * pos, hipMemcpyHostToDevice, stream)) !=
+  int64_t listed = 0;
+  for (int c = 0; c < ncls; ++c) listed += b.count[c];
+  std::copy(work_list.begin(), work_list.begin() + listed, sim->h_work);
+  if (listed > 0) {
+    if ((e = hipMemcpyAsync(sim->d_work, sim->h_work, sizeof(int32_t) * listed, hipMemcpyHostToDevice, stream)) !=
         hipSuccess)
       return hip_fail(e, "hipMemcpyAsync(work)");
     if ((e = hipEventRecord(sim->upload_done, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     sim->upload_pending = true;
   }
 
-  char* sc = sim->d_scratch;
-  rt::SimArgs a;
-  a.points = sim->d_points;
-  a.offsets = trace->offsets;
-  a.param_point = trace->param_point;
-  a.arrival = trace->arrival_ns;
-  a.plen = trace->prompt_len;
-  a.olen = trace->out_len;
-  a.ohat = trace->pred_out_len;
-  a.cls = trace->slo_class;
-  a.samp = trace->sample_bits;
-  a.i_pre = out->i_pre;
-  a.i_dec = out->i_dec;
-  a.ttft = out->ttft_ns;
-  a.span = out->decode_span_ns;
-  // record planes by record size: index 0 of each pool's plane
-  char* rec_planes[2][2] = {{nullptr, nullptr}, {nullptr, nullptr}};
-  for (int k = 0; k < 2 && sc; ++k) {
-    if (any_plain) rec_planes[0][k] = sc + k * plain_plane + ((size_t)rt::kDummyRecords << rt::rec_shift(false));
-    if (any_ledger)
-      rec_planes[1][k] = sc + 2 * plain_plane + k * ledger_plane + ((size_t)rt::kDummyRecords << rt::rec_shift(true));
-  }
-  a.rec[0] = a.rec[1] = nullptr;
-  a.flag = sim->d_flag;
+  char* planes[2][2];
+  const rt::SimArgs a = sim_args(sim, trace, out, L, sim->d_scratch, planes);
   if (sim->timing) {
     if ((st = collect_timing(sim)) != RT_OK) return st;
     if ((e = hipEventRecord(sim->t0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   }
-  // Kernel classes with work, largest first; more than one run side by side
+  // Kernel classes with work, dearest first; more than one run side by side
   // on internal streams forked from and joined back into `stream`.
-  std::vector<int> act;
-  std::vector<double> cost(ncls, 0.0);
-  for (int c = 0; c < ncls; ++c) {
-    if (buckets[c].empty()) continue;
-    act.push_back(c);
-    for (int32_t r : buckets[c]) cost[c] += (double)(off[r + 1] - off[r]) * rt::sim_class(c).S;
-  }
-  std::stable_sort(act.begin(), act.end(), [&](int x, int y) { return cost[x] > cost[y]; });
-  if (act.size() > 1) {
-    while (sim->lanes.size() < act.size()) {
+  const size_t nact = (size_t)b.n_act;
+  if (nact > 1) {
+    while (sim->lanes.size() < nact) {
       hipStream_t l = nullptr;
       hipEvent_t j = nullptr;
       if ((e = hipStreamCreateWithFlags(&l, hipStreamNonBlocking)) != hipSuccess) return hip_fail(e, "hipStreamCreate");
@@ -550,29 +688,106 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
       return hip_fail(e, "hipEventCreate");
     if ((e = hipEventRecord(sim->fork, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   }
-  for (size_t k = 0; k < act.size(); ++k) {
-    const int c = act[k];
-    a.work = sim->d_work + start[c];
-    a.n_work = (int64_t)buckets[c].size();
-    const int lg = rt::mode_ledger(rt::sim_class(c).mode) ? 1 : 0;
-    a.rec[0] = rec_planes[lg][0];
-    a.rec[1] = rec_planes[lg][1];
+  for (size_t k = 0; k < nact; ++k) {
     hipStream_t where = stream;
-    if (act.size() > 1) {
+    if (nact > 1) {
       where = sim->lanes[k];
       if ((e = hipStreamWaitEvent(where, sim->fork, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
     }
-    e = rt::sim_class(c).kind == rt::kBat ? rt::launch_bat(rt::sim_class(c), a, bs[c], where)
-                                          : rt::launch_sim(rt::sim_class(c), a, where);
-    if (e != hipSuccess) return hip_fail(e, "launch(sim)");
-    if (act.size() > 1 && (e = hipEventRecord(sim->joins[k], where)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if ((e = launch_class(b.act[k], a, b, sim->d_work, planes, bs.data(), where)) != hipSuccess)
+      return hip_fail(e, "launch(sim)");
+    if (nact > 1 && (e = hipEventRecord(sim->joins[k], where)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   }
   // The joins go in after every launch: streams share the device's few
   // hardware queues, and a wait enqueued between two launches could hold
   // back a later launch that landed on the same queue.
-  if (act.size() > 1)
-    for (size_t k = 0; k < act.size(); ++k)
+  if (nact > 1)
+    for (size_t k = 0; k < nact; ++k)
       if ((e = hipStreamWaitEvent(stream, sim->joins[k], 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent");
+  if (sim->timing) {
+    if ((e = hipEventRecord(sim->t1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    sim->timed_pending = true;
+  }
+  return RT_OK;
+}
+
+// Host-side planning storage of rt_sim_run_replicas_noalloc, fixed in size
+// and shared by every call (guarded by g_noalloc_mu).
+struct NoAllocHost {
+  int64_t off[kNoAllocMaxReplicas + 1];
+  int32_t pp[kNoAllocMaxReplicas];
+  int32_t work[kNoAllocMaxReplicas];
+  int64_t reps_of[kNoAllocMaxPoints];
+  int choice[kNoAllocMaxPoints], wider[kNoAllocMaxPoints];
+  int64_t count[kMaxClassSlots], start[kMaxClassSlots];
+  double cost[kMaxClassSlots];
+  int act[kMaxClassSlots];
+};
+static NoAllocHost g_noalloc;
+static std::mutex g_noalloc_mu;
+
+rt_status rt_sim_run_replicas_noalloc(rt_sim* sim, const rt_trace* trace, rt_sim_out* out, void* hip_stream) {
+  const char* fn = "rt_sim_run_replicas_noalloc";
+  rt_status st = check_trace(sim, trace, out, fn);
+  if (st != RT_OK || trace->n_replicas == 0) return st;
+  if (trace->n_requests > 0 && (!out->i_pre || !out->i_dec)) return fail(RT_EINVAL, std::string(fn) + ": null placement output");
+  if (trace->n_replicas > kNoAllocMaxReplicas)
+    return fail(RT_ERANGE, std::string(fn) + ": more than " + std::to_string(kNoAllocMaxReplicas) + " replicas");
+  if ((int64_t)sim->points.size() > kNoAllocMaxPoints)
+    return fail(RT_ERANGE, std::string(fn) + ": simulator has more than " + std::to_string(kNoAllocMaxPoints) +
+                               " points");
+  if (rt::sim_class_count() > kMaxClassSlots) return fail(RT_EDEVICE, std::string(fn) + ": class table overflow");
+  if (!sim->static_scratch) return fail(RT_EDEVICE, std::string(fn) + ": static scratch not resolved");
+  DeviceScope ds(sim->device);
+  if (ds.err != hipSuccess) return hip_fail(ds.err, "hipSetDevice");
+  hipStream_t stream = (hipStream_t)hip_stream;
+  const int64_t n = trace->n_replicas;
+  std::lock_guard<std::mutex> lk(g_noalloc_mu);
+  NoAllocHost& h = g_noalloc;
+  hipError_t e = hipMemcpyAsync(h.off, trace->offsets, sizeof(int64_t) * (n + 1), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) {
+    if (trace->param_point)
+      e = hipMemcpyAsync(h.pp, trace->param_point, sizeof(int32_t) * n, hipMemcpyDeviceToHost, stream);
+    else
+      std::fill(h.pp, h.pp + n, 0);
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_fail(e, "reading offsets/param_point");
+  if ((st = check_plan_inputs(sim, trace, h.off, h.pp, fn)) != RT_OK) return st;
+  PlanBufs b{h.off, h.pp, h.reps_of, h.choice, h.wider, h.count, h.start, h.cost, h.work, h.act, 0};
+  plan_launch(rt_sim_points{sim->points.size(), sim->point_classes.data()}, n, b);
+  if ((st = check_sample_bits(sim, trace, b, fn)) != RT_OK) return st;
+  for (int k = 0; k < b.n_act; ++k)
+    if (rt::sim_class(b.act[k]).kind == rt::kBat)
+      return fail(RT_EUNSUPPORTED, std::string(fn) + ": continuous-batching points need rt_sim_run_replicas");
+  // static scratch: the record planes, then the work list
+  const RecLayout L = rec_layout(b, (size_t)trace->n_requests);
+  int64_t listed = 0;
+  for (int k = 0; k < b.n_act; ++k) listed += b.count[b.act[k]];
+  const size_t need = L.bytes + sizeof(int32_t) * (size_t)listed;
+  if (need > kStaticScratchBytes)
+    return fail(RT_ERANGE, std::string(fn) + ": needs " + std::to_string(need) + " bytes of scratch, more than its " +
+                               std::to_string(kStaticScratchBytes) + " (64 bytes per request, 128 with the proxy "
+                               "backlog, 192 when a call holds both, + 4 per replica)");
+  char* base = (char*)sim->static_scratch;
+  int32_t* d_work = (int32_t*)(base + L.bytes);
+  // the work list is copied before the host array can be planned over again
+  if (listed > 0) {
+    if ((e = hipMemcpyAsync(d_work, h.work, sizeof(int32_t) * listed, hipMemcpyHostToDevice, stream)) != hipSuccess)
+      return hip_fail(e, "hipMemcpyAsync(work)");
+    if ((e = hipEventRecord(sim->upload_done, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if ((e = hipEventSynchronize(sim->upload_done)) != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  }
+  char* planes[2][2];
+  const rt::SimArgs a = sim_args(sim, trace, out, L, base, planes);
+  if (sim->timing) {
+    if ((st = collect_timing(sim)) != RT_OK) return st;
+    if ((e = hipEventRecord(sim->t0, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
+  // every class on the caller's stream, dearest first (no internal streams)
+  for (int k = 0; k < b.n_act; ++k)
+    if ((e = launch_class(b.act[k], a, b, d_work, planes, nullptr, stream)) != hipSuccess)
+      return hip_fail(e, "launch(sim)");
   if (sim->timing) {
     if ((e = hipEventRecord(sim->t1, stream)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     sim->timed_pending = true;

@@ -27,8 +27,8 @@ RT_SERVICE = {"serial": 0, "batched": 1}
 RT_MAX_CLASSES = 8
 RT_MAX_POOL = 1024
 
-EXPORTS = ("rt_sim_create", "rt_sim_destroy", "rt_sim_run_replicas", "rt_goodput", "rt_sim_data_status",
-           "rt_sim_timing", "rt_sim_kernel_time", "rt_score_argmin", "rt_last_error")
+EXPORTS = ("rt_sim_create", "rt_sim_destroy", "rt_sim_run_replicas", "rt_sim_run_replicas_noalloc", "rt_goodput",
+           "rt_sim_data_status", "rt_sim_timing", "rt_sim_kernel_time", "rt_score_argmin", "rt_last_error")
 
 
 class RtError(RuntimeError):
@@ -78,6 +78,7 @@ def _load():
     L.rt_sim_create.argtypes = [C.POINTER(rt_point), C.c_int32, C.c_int32, C.POINTER(C.c_void_p)]
     L.rt_sim_destroy.argtypes = [P]
     L.rt_sim_run_replicas.argtypes = [P, C.POINTER(rt_trace), C.POINTER(rt_sim_out), P]
+    L.rt_sim_run_replicas_noalloc.argtypes = [P, C.POINTER(rt_trace), C.POINTER(rt_sim_out), P]
     L.rt_goodput.argtypes = [P, C.POINTER(rt_trace), C.POINTER(rt_sim_out), P, P, P]
     L.rt_sim_data_status.argtypes = [P, P, C.POINTER(C.c_uint32)]
     L.rt_sim_timing.argtypes = [P, C.c_int32]
@@ -204,6 +205,12 @@ def _out_struct(out: Dict[str, torch.Tensor]) -> rt_sim_out:
 def rt_sim_run_replicas(sim: int, trace: Dict[str, torch.Tensor], out: Dict[str, torch.Tensor], stream=None) -> None:
     t, o = _trace_struct(trace), _out_struct(out)
     _check(_lib.rt_sim_run_replicas(sim, C.byref(t), C.byref(o), _stream(stream)))
+
+
+def rt_sim_run_replicas_noalloc(sim: int, trace: Dict[str, torch.Tensor], out: Dict[str, torch.Tensor],
+                                stream=None) -> None:
+    t, o = _trace_struct(trace), _out_struct(out)
+    _check(_lib.rt_sim_run_replicas_noalloc(sim, C.byref(t), C.byref(o), _stream(stream)))
 
 
 def rt_goodput(sim: int, trace: Dict[str, torch.Tensor], out: Dict[str, torch.Tensor], goodput: torch.Tensor,

@@ -99,6 +99,7 @@ def test_sim_argument_errors(rt):
     pt = (rt.rt_point * 1)()
     assert L.rt_sim_create(pt, 0, 0, C.byref(h)) == rt.RT_EINVAL
     assert L.rt_sim_run_replicas(None, None, None, None) == rt.RT_EINVAL
+    assert L.rt_sim_run_replicas_noalloc(None, None, None, None) == rt.RT_EINVAL
     assert L.rt_goodput(None, None, None, None, None, None) == rt.RT_EINVAL
     assert L.rt_sim_data_status(None, None, None) == rt.RT_EINVAL
     assert L.rt_sim_timing(None, 1) == rt.RT_EINVAL
