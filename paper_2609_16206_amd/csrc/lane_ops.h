@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace rt {
 
 constexpr double kTwo32 = 4294967296.0;
@@ -33,6 +35,19 @@ template <typename T>
 __device__ __forceinline__ T opaque(T x) {
   asm("" : "+v"(x));
   return x;
+}
+
+// Calls f(std::integral_constant<int, I>) for I = 0 .. N-1, so that code
+// acting on register-resident slots under a branch indexes them with
+// constants from the start (a loop index is constant only after unrolling,
+// and the optimizer may turn such code into an access at a computed index
+// first, which moves the slots to scratch memory).
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
 }
 
 // ---------------------------------------------------------------------------

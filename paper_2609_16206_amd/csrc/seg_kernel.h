@@ -36,15 +36,23 @@
 //
 // FIFO of in-flight requests per instance.  Service is in admission order,
 // so an instance releases its requests in admission order.  The first three
-// requests of each FIFO are kept in registers; the rest is a list in HBM
-// scratch in which every request's record holds its first and second
-// successor (release time, index, cache tokens: one 32-byte sector; ledger
-// tokens after them in the modes that price the ledger), written when those
-// successors are admitted.  Up to two releases per instance between two
-// arrivals shift the register window, and the new
-// head's two successors are then loaded with one independent access (no
-// chain of dependent loads), merged at the end of the step; a third release
-// in one step takes the slow path, which waits.
+// requests of each FIFO (positions 0, 1, 2) are kept in registers; the rest
+// is a list in HBM scratch in which a request's record holds its first and
+// second successor (release time, index, cache tokens: one 32-byte sector;
+// ledger tokens after them in the modes that price the ledger).  Records are
+// written only when a request joins beyond the register window (position
+// 3 or later): it is then stored as the first successor of the request
+// ahead of it and as the second successor of the one ahead of that.  So the
+// record of the request at position p holds a valid first successor when
+// p >= 2 and a valid second successor when p >= 1 (where those successors
+// exist), and a FIFO that never grows past three requests never touches
+// scratch.  Up to two releases per instance between two arrivals shift the
+// register window; the positions the shift leaves empty are then filled
+// from the new head's record, loaded with one independent access (no chain
+// of dependent loads) and merged at the end of the step: after one release
+// only position 2 (the new head's second successor), after two releases
+// positions 1 and 2.  A third release in one step takes the slow path,
+// which waits.
 //
 // Memory ordering within a step (one wave): on gfx9 loads and stores share
 // one counter, so a wait for a load also waits for every older store.  The
@@ -94,7 +102,8 @@ struct Slot {
   int32_t tail2;    // the one admitted before it
   Elem h, n, n2;    // FIFO positions 0, 1, 2 (t = +inf beyond the FIFO)
   Elem l1, l2;      // successors of the head, loaded this step
-  int32_t lq;       // FIFO length the loaded pair describes (0: nothing loaded)
+  int32_t lq;       // positions the loaded pair fills: bit 0 position 1,
+                    // bit 1 position 2 (0: nothing loaded)
 };
 
 __device__ __forceinline__ Elem none() { return Elem{kInf, 0, 0, 0}; }
@@ -112,10 +121,9 @@ __device__ __forceinline__ Elem sel(bool c, const Elem& x, const Elem& y) {
   return Elem{c ? x.t : y.t, c ? x.idx : y.idx, c ? x.fp : y.fp, c ? x.pt : y.pt};
 }
 
-// The loaded successors fill positions 1 and 2 where the FIFO (as it was
-// when they were loaded) reaches them.
+// The loaded successors fill the positions the last release left empty.
 __device__ __forceinline__ void merge_pending(Slot& s) {
-  const bool m1 = s.lq >= 2, m2 = s.lq >= 3;
+  const bool m1 = (s.lq & 1) != 0, m2 = (s.lq & 2) != 0;
   s.n = sel(m1, s.l1, s.n);
   s.n2 = sel(m2, s.l2, s.n2);
   s.lq = 0;
@@ -201,13 +209,18 @@ __device__ __forceinline__ void sample_pair(uint32_t u, uint32_t v, uint32_t n, 
   c2 = n > 1 ? x + (x >= c1 ? 1u : 0u) : c1;
 }
 
-// Release: up to two completions per instance from the register window; the
-// new head's successors are loaded unconditionally (the wave's dummy record
-// `dmy` when there is nothing to load) and merged later.  `recr` is the
-// lane's record plane at its replica's request 0; indices are relative to
-// it (the dummy's too), so that an address is one shift-add.
+// Which window positions the new head's record must fill after a release
+// (p1: one request released, p2: two), with q requests left: bit 0 position
+// 1 (only after two releases), bit 1 position 2.
+__device__ __forceinline__ int32_t refill_mask(bool p1, bool p2, int32_t q) {
+  return (p2 && q >= 2 ? 1 : 0) | (p1 && q >= 3 ? 2 : 0);
+}
+
+// Release without the refill: up to two completions per instance from the
+// register window; records in x.lq which positions the new head's record
+// must fill (refill_mask).
 template <bool kTok, bool kKv>
-__device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char* recr, int32_t R, int64_t dmy) {
+__device__ __forceinline__ void release_pop(Slot& x, double now_eff) {
   const bool p1 = x.h.t <= now_eff;
   const bool p2 = x.n.t <= now_eff;  // implies p1 (release times do not decrease)
   x.q -= (p1 ? 1 : 0) + (p2 ? 1 : 0);
@@ -219,11 +232,24 @@ __device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char
   x.h = h1;
   x.n = n1;
   x.n2.t = p1 ? kInf : x.n2.t;
-  const int32_t lq = opaque(p1 ? x.q : 0);
-  const bool ld = lq >= 2;
-  const int64_t g = sel_index(ld, min(max(x.h.idx, 0), max(R - 1, 0)), dmy);
+  x.lq = opaque(refill_mask(p1, p2, x.q));
+}
+
+// The refill load of a released slot: the new head's record where x.lq asks
+// for one, else the wave's dummy record `dmy`.  `recr` is the lane's record
+// plane at its replica's request 0; indices are relative to it (the
+// dummy's too), so that an address is one shift-add.
+template <bool kTok>
+__device__ __forceinline__ void load_refill(Slot& x, const char* recr, int32_t R, int64_t dmy) {
+  const int64_t g = sel_index(x.lq != 0, min(max(x.h.idx, 0), max(R - 1, 0)), dmy);
   load_pair<kTok>(x, rec_at<kTok>(recr, g));
-  x.lq = lq;
+}
+
+// Release with its refill load issued unconditionally, merged later.
+template <bool kTok, bool kKv>
+__device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char* recr, int32_t R, int64_t dmy) {
+  release_pop<kTok, kKv>(x, now_eff);
+  load_refill<kTok>(x, recr, R, dmy);
 }
 
 template <int M, bool kTok, bool kKv>
@@ -466,7 +492,7 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     const int32_t wl = go ? (isp ? wp : wd) : -1;
     const bool own_lane = opaque(wl) == sl;
     const int32_t wm = own_lane ? (isp ? mp : md) : -1;
-    int32_t st1 = -1, st2 = -1;  // requests whose first / second successor is z
+    int32_t st1 = -1, st2 = -1;  // requests whose first / second successor is z (z beyond the window)
 #pragma unroll
     for (int m = 0; m < M; ++m) {
       Slot& x = s[m];
@@ -475,8 +501,8 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
       x.h = sel(w == 0, z, x.h);
       x.n = sel(w == 1, z, x.n);
       x.n2 = sel(w == 2, z, x.n2);
-      st1 = w >= 1 ? x.tail : st1;
-      st2 = w >= 2 ? x.tail2 : st2;
+      st1 = w >= 3 ? x.tail : st1;
+      st2 = w >= 3 ? x.tail2 : st2;
       x.tail2 = own ? x.tail : x.tail2;
       x.tail = own ? t : x.tail;
       x.q = own ? x.q + 1 : x.q;

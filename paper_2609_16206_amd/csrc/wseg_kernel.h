@@ -3,8 +3,8 @@
 //
 // Method and per-instance machinery as in seg_kernel.h (Algorithm 1 per
 // admission on the serial-service simulator of Section III-D / Section VI;
-// Section III-A costs; the register FIFO window with two-successor records;
-// the rotated step).  Differences for wide pools:
+// Section III-A costs; the register FIFO window with successor records
+// written only beyond the window).  Differences for wide pools:
 //
 // Mapping.  One replica per workgroup of W waves.  Instances are dealt to the
 // waves round robin (instance j of a pool to wave j mod W), so that runs of
@@ -16,16 +16,27 @@
 //
 // Argmin.  Each wave reduces both pools over its 64 lanes (DPP + readlane;
 // within a wave the lowest lane and slot hold the lowest index), then lane 0
-// of every wave publishes its two winners (and the prefill winner's
-// busy-until) in LDS; after one barrier every wave combines them by (cost,
-// index), so equal costs keep the lowest index.  The LDS slots are
-// double-buffered by step parity, so one barrier per step suffices.
+// of every wave folds its two winners into an LDS minimum of the packed key
+// (cost key << 32 | instance index), so equal costs keep the lowest index,
+// and writes their busy-until next to it.  After one barrier per step every
+// wave reads both minima and the two winners' busy-until, so all waves form
+// the same prefill and decode ends.  The LDS cells rotate over three step
+// slots: slot t % 3 is filled at step t, read after its barrier, and reset by
+// wave 0 after the barrier of step t + 1 (every wave has read it by then, and
+// none writes it again before the barrier of step t + 2).
 //
-// Sparse work.  Per step only the two winning instances are appended to and
-// only instances whose head has finished are released, so both run under
-// uniform branches: the append in the winner's wave and only for the
-// winner's slot, the release only for slots where some lane's head has
-// finished.
+// Per-step work is kept to one vector compare and one uniform branch per
+// phase where it is usually idle: the merge of refill loads runs only for
+// slots that issued one (a scalar mask), the releases only when some head of
+// the wave has finished, the slow path only when a head is still finished
+// after them, and the appends, whose FIFO position is the winner's queue
+// length read as a scalar, touch scratch only beyond the register window.
+//
+// Requests and outcomes move in blocks of 64: lane k of every wave holds the
+// features of request (block start + k), loaded one block ahead with one
+// coalesced load per field, and a step reads its request with readlane;
+// wave 0's lane k keeps the outcome of step (block start + k) and the block
+// is written with one coalesced store per output array.
 #pragma once
 
 #include "seg_kernel.h"
@@ -37,8 +48,20 @@ namespace seg {
 // at M per lane.
 __host__ __device__ inline int wide_pool_lanes(int n, int M, int W) { return ((n + W - 1) / W + M - 1) / M; }
 
+__device__ __forceinline__ double rl_f64(double v, int lane) {
+  return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(v), lane),
+                          __builtin_amdgcn_readlane(__double2loint(v), lane));
+}
+
+__device__ __forceinline__ int64_t rl_i64(int64_t v, int lane) {
+  return (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int32_t)(v >> 32), lane) << 32) |
+                   (uint32_t)__builtin_amdgcn_readlane((int32_t)v, lane));
+}
+
 template <int W, int M, int kMode>
 __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
+  static_assert(W == 2 || W == 4 || W == 8, "workgroups of 2, 4 or 8 waves");
+  constexpr int kLogW = W == 2 ? 1 : (W == 4 ? 2 : 3);
   constexpr bool kTok = mode_ledger(kMode);    // the ledger is priced
   constexpr bool kKv = kMode != kModeBase;     // occupancy is priced
   constexpr bool kSamp = mode_sampled(kMode);  // two candidates per pool
@@ -65,6 +88,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   const float basec = isp ? pt.pre_base : 0.0f;  // proxy ledger: base per in-flight prefill
   const double pre_base_ns = (double)pt.pre_base_ns, pre_tok_ns = (double)pt.pre_tok_ns;
   const double dec_tok_ns = (double)pt.dec_tok_ns, xfer_tok_ns = (double)pt.xfer_tok_ns;
+  const float sigv = pt.sigma[lane & (kMaxClasses - 1)];  // lane k: sigma of class k mod 8
   char* const recb = isp ? a.rec[0] : a.rec[1];
   const uint32_t wave_id = (blockIdx.x * W + wave) & (kDummyRecords - 1);
   // the lane's plane at its replica's request 0; the wave's dummy record,
@@ -72,14 +96,9 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   char* const recr = recb + rec_off<kTok>(base);
   const int64_t dmy = -1 - (int64_t)wave_id - base;
 
-  struct Part {
-    uint32_t kp, kd;  // the wave's best prefill / decode key
-    int32_t ip, id;   // their instance indices
-    double bp;        // busy-until of the wave's best prefill instance
-  };
-  __shared__ float sig[kMaxClasses];
-  __shared__ Part part[2][W];
-  if (threadIdx.x < kMaxClasses) sig[threadIdx.x] = pt.sigma[threadIdx.x];
+  __shared__ unsigned long long best[3][2];  // per step slot: packed minimum of each pool
+  __shared__ double wbusy[3][W][2];          // per step slot: each wave's winners' busy-until
+  if (threadIdx.x < 6) best[threadIdx.x >> 1][threadIdx.x & 1] = ~0ull;
   __syncthreads();
 
   Slot s[M];
@@ -90,38 +109,64 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     ok[m] = inpool && wave + W * (lrel * M + m) < npool;
   }
 
-  // request 0 (nothing to release yet); the features of request 1 in flight
-  double last_now = 0.0;
-  Req cur = admit_check(R, ncls, a.arrival[base], a.plen[base], a.olen[base], a.ohat[base], a.cls[base], last_now);
-  float sg = sig[a.cls[base] & (kMaxClasses - 1)];
-  // the candidate words of the lane's pool (sampled modes)
-  auto load_words = [&](int64_t g, uint32_t& u, uint32_t& v) {
+  // Features of a block of 64 requests, lane k holding request (block + k)
+  // (clamped into the replica).
+  struct Block {
+    int64_t arr;
+    int32_t p, o, oh;
+    uint32_t c;
+    uint32_t w[4];  // candidate words (sampled modes)
+  };
+  auto load_block = [&](Block& f, int32_t blk) __attribute__((always_inline)) {
+    const int64_t g = base + min(blk + lane, R - 1);
+    f.arr = a.arrival[g];
+    f.p = a.plen[g];
+    f.o = a.olen[g];
+    f.oh = a.ohat[g];
+    f.c = a.cls[g];
     if constexpr (kSamp) {
-      const uint2 w = *reinterpret_cast<const uint2*>(a.samp + 4 * g + (isp ? 0 : 2));
-      u = w.x;
-      v = w.y;
+      const uint4 w = *reinterpret_cast<const uint4*>(a.samp + 4 * g);
+      f.w[0] = w.x;
+      f.w[1] = w.y;
+      f.w[2] = w.z;
+      f.w[3] = w.w;
     } else {
-      u = v = 0;
+      f.w[0] = f.w[1] = f.w[2] = f.w[3] = 0;
     }
   };
-  uint32_t cu, cv;
-  load_words(base, cu, cv);
-  const int32_t last = R - 1;
-  int64_t nx_arr;
-  int32_t nx_p, nx_o, nx_oh;
-  uint32_t nx_c, nx_u, nx_v;
-  {
-    const int64_t g = base + min(1, last);
-    nx_arr = a.arrival[g];
-    nx_p = a.plen[g];
-    nx_o = a.olen[g];
-    nx_oh = a.ohat[g];
-    nx_c = a.cls[g];
-    load_words(g, nx_u, nx_v);
-  }
-  int32_t rr = 0;     // round robin: t mod (size of this lane's pool)
-  double tmax = 0.0;  // latest decode end this lane recorded (time-range check)
-  uint32_t rej = 0;   // a rejected request was recorded by this lane
+  Block fb0, fb1;  // the current block and the next
+  load_block(fb0, 0);
+  load_block(fb1, 64);
+
+  double last_now = 0.0;  // latest accepted arrival (arrivals must not decrease)
+  float sg;               // sigma of the current request's class
+  uint32_t cu = 0, cv = 0;  // the lane's pool's candidate words of the current request
+  // Request k of the current block, checked against the replica (its
+  // features are uniform: read from lane k).
+  auto take = [&](int k, int32_t t) __attribute__((always_inline)) {
+    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.c, k);
+    sg = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int32_t, sigv), (int)(c & 7u)));
+    if constexpr (kSamp) {
+      const uint32_t w0 = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.w[0], k);
+      const uint32_t w1 = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.w[1], k);
+      const uint32_t w2 = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.w[2], k);
+      const uint32_t w3 = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.w[3], k);
+      cu = isp ? w0 : w2;
+      cv = isp ? w1 : w3;
+    }
+    return admit_check(R - t, ncls, rl_i64(fb0.arr, k), __builtin_amdgcn_readlane(fb0.p, k),
+                       __builtin_amdgcn_readlane(fb0.o, k), __builtin_amdgcn_readlane(fb0.oh, k), c, last_now);
+  };
+  Req cur = take(0, 0);
+
+  // outcomes of the current block (wave 0, lane k: step block start + k)
+  int32_t b_ip = -1, b_id = -1;
+  int64_t b_tt = -1, b_sp = -1;
+  int32_t rr = 0;      // round robin: t mod (size of this lane's pool)
+  double tmax = 0.0;   // latest decode end (time-range check)
+  bool rej = false;    // a request was rejected
+  uint32_t pend = 0;   // slots whose refill load is in flight (bit m)
+  int sl3 = 0;         // step slot t % 3 of the LDS cells
 
   for (int32_t t = 0; t < R; ++t) {
     const int32_t p = cur.p, o = cur.o, oh = cur.oh, po = cur.po, poh = cur.poh;
@@ -176,7 +221,8 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
       }
     }
 
-    // 2. per-wave argmin of both pools, then across waves through LDS
+    // 2. per-wave argmin of both pools; lane 0 folds the wave's winners into
+    // the LDS minima and publishes their busy-until
     {
       uint32_t kp = isp ? bkey : 0xffffffffu, kd = isp ? 0xffffffffu : bkey;
       const uint32_t kp0 = kp, kd0 = kd;
@@ -185,168 +231,148 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
       const int32_t wd = seg_first<64>(kd0 == kd, lane) & 63;
       const int32_t mpw = __builtin_amdgcn_readlane(bm, wp);
       const int32_t mdw = __builtin_amdgcn_readlane(bm, wd);
-      const double bpw = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(bbusy), wp),
-                                          __builtin_amdgcn_readlane(__double2loint(bbusy), wp));
-      if (lane == 0)
-        part[t & 1][wave] = Part{kp, kd, wave + W * (wp * M + mpw), wave + W * ((wd - LPW) * M + mdw), bpw};
+      const double bpw = rl_f64(bbusy, wp), bdw = rl_f64(bbusy, wd);
+      const uint32_t ipw = (uint32_t)(wave + W * (wp * M + mpw));
+      const uint32_t idw = (uint32_t)(wave + W * ((wd - LPW) * M + mdw));
+      if (lane == 0) {
+        atomicMin(&best[sl3][0], ((unsigned long long)kp << 32) | ipw);
+        atomicMin(&best[sl3][1], ((unsigned long long)kd << 32) | idw);
+        wbusy[sl3][wave][0] = bpw;
+        wbusy[sl3][wave][1] = bdw;
+      }
     }
     __syncthreads();
-    uint32_t kp = part[t & 1][0].kp, kd = part[t & 1][0].kd;
-    int32_t ip = part[t & 1][0].ip, id = part[t & 1][0].id;
-    double busy_ip = part[t & 1][0].bp;
+    const int32_t ip = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)best[sl3][0]);
+    const int32_t id = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)best[sl3][1]);
+    double busy_ip = wbusy[sl3][0][0], busy_id = wbusy[sl3][0][1];
 #pragma unroll
     for (int w = 1; w < W; ++w) {
-      const Part x = part[t & 1][w];
-      const bool bp = x.kp < kp || (x.kp == kp && x.ip < ip);
-      const bool bd = x.kd < kd || (x.kd == kd && x.id < id);
-      kp = bp ? x.kp : kp;
-      ip = bp ? x.ip : ip;
-      busy_ip = bp ? x.bp : busy_ip;
-      kd = bd ? x.kd : kd;
-      id = bd ? x.id : id;
+      busy_ip = (ip & (W - 1)) == w ? wbusy[sl3][w][0] : busy_ip;
+      busy_id = (id & (W - 1)) == w ? wbusy[sl3][w][1] : busy_id;
     }
-    ip = __builtin_amdgcn_readfirstlane(ip);
-    id = __builtin_amdgcn_readfirstlane(id);
+    // the cells of step t - 1 are free again (every wave has read them)
+    const int sl_prev = sl3 == 0 ? 2 : sl3 - 1;
+    if (wave == 0 && lane < 2) best[sl_prev][lane] = ~0ull;
 
-    // 3. serve (uniform up to the decode winner's own busy-until); the
-    // winners' waves, lanes and slots
+    // 3. serve (uniform): prefill, KV transfer, decode (exact integers in
+    // doubles)
     const double s_pre = __builtin_fma((double)p, pre_tok_ns, pre_base_ns);
     const double pf_end = __builtin_fmax(now, busy_ip) + s_pre;
     const double kv_at = pf_end + (double)p * xfer_tok_ns;
-    const int32_t wpo = ip % W, wdo = id % W;            // waves
-    const int32_t qp = ip / W, qd = id / W;              // positions within the wave
-    const int32_t lpo = qp / M, ldo = LPW + qd / M;      // lanes
-    const int32_t mp = qp - (qp / M) * M, md = qd - (qd / M) * M;  // slots
+    const double de = __builtin_fmax(kv_at, busy_id) + (double)(o - 1) * dec_tok_ns;
 
-    // 4. the successors loaded during request t's releases (slots where any
-    // lane loaded some; every slot's test is made before the first branch,
-    // so that the scalar branches wait for one vector compare, not one each)
-    {
-      uint64_t any_lq[M];
-#pragma unroll
-      for (int m = 0; m < M; ++m) any_lq[m] = __ballot(s[m].lq >= 2);
-#pragma unroll
-      for (int m = 0; m < M; ++m)
-        if (any_lq[m]) merge_pending(s[m]);
+    // 4. refill loads of request t's releases, where any were issued
+    if (pend) {
+      static_for<M>([&](auto mc) __attribute__((always_inline)) {
+        if (pend & (1u << decltype(mc)::value)) merge_pending(s[decltype(mc)::value]);
+      });
+      pend = 0;
     }
 
-    // 5. request t+1: check and sigma (its features are waited for here,
-    // ahead of the stores below, which the compiler's waits do not count)
-    const Req nxt = [&] {
-      // (uniform over the workgroup; reading the first lane tells the compiler)
-      const int64_t u_arr = ((int64_t)__builtin_amdgcn_readfirstlane((int32_t)(nx_arr >> 32)) << 32) |
-                            (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)nx_arr);
-      const uint32_t u_c = (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)nx_c);
-      sg = sig[u_c & (kMaxClasses - 1)];
-      return admit_check(R - (t + 1), ncls, u_arr, __builtin_amdgcn_readfirstlane(nx_p),
-                         __builtin_amdgcn_readfirstlane(nx_o), __builtin_amdgcn_readfirstlane(nx_oh), u_c, last_now);
-    }();
-
-    // 6. append the request to the winning slot of each pool (uniform
-    // branches: the winner's wave, the winner's slot) and record the outcome;
-    // only the lanes with something to store store it.  Addresses stay inside
-    // the plane on every lane: a tail is >= -1, and index -1 is the record
-    // before the replica's first (a dummy record for the trace's first).
-    if (go && wave == wpo) {
-      const Elem z{pf_end, t, p, p};
-      const u32x4 zv = {(uint32_t)__double2loint(pf_end), (uint32_t)__double2hiint(pf_end), (uint32_t)t, (uint32_t)p};
-#pragma unroll
-      for (int m = 0; m < M; ++m)
-        if (m == mp) {
+    // 5. append the request to the winning slot of each pool (uniform
+    // branches: the winner's wave and slot, then its FIFO position)
+    if (go) {
+      auto append = [&](int32_t win, int32_t lane_off, double end, int32_t fp, int32_t tk) __attribute__((always_inline)) {
+        const int32_t q = win >> kLogW;       // position within the wave
+        const int32_t lw = lane_off + q / M;  // lane
+        const int32_t mw = q - (q / M) * M;  // slot
+        const bool own = lane == lw;
+        const Elem z{end, t, fp, tk};
+        static_for<M>([&](auto mc) __attribute__((always_inline)) {
+          constexpr int m = decltype(mc)::value;
+          if (m != mw) return;
           Slot& x = s[m];
-          const bool own = lane == lpo;
-          const int32_t w = opaque(own ? x.q : -1);  // z's FIFO position
-          x.h = sel(w == 0, z, x.h);
-          x.n = sel(w == 1, z, x.n);
-          x.n2 = sel(w == 2, z, x.n2);
-          const uint32_t s1 = opaque(w) >= 1 ? 1u : 0u, s2 = opaque(w) >= 2 ? 1u : 0u;
-          const int64_t g1 = x.tail, g2 = x.tail2;
-          x.tail2 = own ? x.tail : x.tail2;
-          x.tail = own ? t : x.tail;
-          x.q = own ? x.q + 1 : x.q;
-          if constexpr (kKv) x.kv = x.kv + (own ? (double)p : 0.0);
-          if constexpr (kTok) x.pend = x.pend + (own ? (double)p : 0.0);
-          x.busy = own ? pf_end : x.busy;
-          if constexpr (kTok) {
-            store_x4_b32_if(s1, recr + rec_off<kTok>(g1), zv, recr + rec_off<kTok>(g1) + kRecTok, (uint32_t)p);
-            store_x4_b32_if(s2, recr + rec_off<kTok>(g2) + 16, zv, recr + rec_off<kTok>(g2) + kRecTok + 4, (uint32_t)p);
-          } else {
-            store_x4_if(s1, recr + rec_off<kTok>(g1), zv);
-            store_x4_if(s2, recr + rec_off<kTok>(g2) + 16, zv);
+          const int32_t w = __builtin_amdgcn_readlane(x.q, lw);  // z's FIFO position
+          if (w == 0) {
+            x.h = sel(own, z, x.h);
+          } else if (w == 1) {
+            x.n = sel(own, z, x.n);
+          } else if (w == 2) {
+            x.n2 = sel(own, z, x.n2);
+          } else if (own) {
+            // beyond the window: z is the first successor of the tail and
+            // the second of the request before it
+            char* const r1 = rec_at<kTok>(recr, x.tail);
+            char* const r2 = rec_at<kTok>(recr, x.tail2);
+            *reinterpret_cast<Entry*>(r1) = Entry{end, t, fp};
+            *reinterpret_cast<Entry*>(r2 + 16) = Entry{end, t, fp};
+            if constexpr (kTok) {
+              *reinterpret_cast<int32_t*>(r1 + kRecTok) = tk;
+              *reinterpret_cast<int32_t*>(r2 + kRecTok + 4) = tk;
+            }
           }
-        }
-    }
-    if (go && wave == wdo) {
-#pragma unroll
-      for (int m = 0; m < M; ++m)
-        if (m == md) {
-          Slot& x = s[m];
-          const bool own = lane == ldo;
-          const double de = __builtin_fmax(kv_at, x.busy) + (double)(o - 1) * dec_tok_ns;
-          const Elem z{de, t, po, oh};
-          const int32_t w = opaque(own ? x.q : -1);
-          x.h = sel(w == 0, z, x.h);
-          x.n = sel(w == 1, z, x.n);
-          x.n2 = sel(w == 2, z, x.n2);
-          const uint32_t s1 = opaque(w) >= 1 ? 1u : 0u, s2 = opaque(w) >= 2 ? 1u : 0u;
-          const int64_t g1 = x.tail, g2 = x.tail2;
-          x.tail2 = own ? x.tail : x.tail2;
-          x.tail = own ? t : x.tail;
+          const int32_t tl_old = x.tail;
+          x.tail2 = own ? tl_old : x.tail2;
+          x.tail = own ? t : tl_old;
           x.q = own ? x.q + 1 : x.q;
-          if constexpr (kKv) x.kv = x.kv + (own ? (double)po : 0.0);
-          if constexpr (kTok) x.pend = x.pend + (own ? (double)oh : 0.0);
-          x.busy = own ? de : x.busy;
-          const u32x4 zv = {(uint32_t)__double2loint(de), (uint32_t)__double2hiint(de), (uint32_t)t, (uint32_t)po};
-          if constexpr (kTok) {
-            store_x4_b32_if(s1, recr + rec_off<kTok>(g1), zv, recr + rec_off<kTok>(g1) + kRecTok, (uint32_t)oh);
-            store_x4_b32_if(s2, recr + rec_off<kTok>(g2) + 16, zv, recr + rec_off<kTok>(g2) + kRecTok + 4, (uint32_t)oh);
-          } else {
-            store_x4_if(s1, recr + rec_off<kTok>(g1), zv);
-            store_x4_if(s2, recr + rec_off<kTok>(g2) + 16, zv);
-          }
-          // the outcome, by the decode winner
-          tmax = __builtin_fmax(tmax, own ? de : 0.0);
-          const int64_t go_i = base + t;
-          store_out_if(own ? 1u : 0u, a.i_pre + go_i, ip, a.i_dec + go_i, id, a.ttft + go_i, f64_to_i64(pf_end - now),
-                       a.span + go_i, f64_to_i64(de - pf_end));
-        }
+          if constexpr (kKv) x.kv = x.kv + (own ? (double)fp : 0.0);
+          if constexpr (kTok) x.pend = x.pend + (own ? (double)tk : 0.0);
+          x.busy = own ? end : x.busy;
+        });
+      };
+      if (wave == (ip & (W - 1))) append(ip, 0, pf_end, p, p);
+      if (wave == (id & (W - 1))) append(id, LPW, de, po, oh);
     }
-    if (!go && wave == 0) {
-      // a rejected request: -1 outputs, by lane 0
-      rej |= lane == 0 ? 1u : 0u;
-      const int64_t go_i = base + t;
-      store_out_if(lane == 0 ? 1u : 0u, a.i_pre + go_i, -1, a.i_dec + go_i, -1, a.ttft + go_i, (int64_t)-1,
-                   a.span + go_i, (int64_t)-1);
+
+    // 6. the outcome, kept by wave 0's lane t mod 64 until its block is
+    // written
+    if (wave == 0) {
+      const bool keep = lane == (t & 63);
+      b_ip = keep ? (go ? ip : -1) : b_ip;
+      b_id = keep ? (go ? id : -1) : b_id;
+      b_tt = keep ? (go ? f64_to_i64(pf_end - now) : -1) : b_tt;
+      b_sp = keep ? (go ? f64_to_i64(de - pf_end) : -1) : b_sp;
+      tmax = go ? __builtin_fmax(tmax, de) : tmax;
+      rej = rej || !go;
+      if ((t & 63) == 63 || t == R - 1) {
+        const int32_t tl = (t & ~63) + lane;
+        if (tl <= t) {
+          const int64_t gi = base + tl;
+          a.i_pre[gi] = b_ip;
+          a.i_dec[gi] = b_id;
+          a.ttft[gi] = b_tt;
+          a.span[gi] = b_sp;
+        }
+      }
     }
     if constexpr (kMode == kModeBase) rr = (rr + 1 == npool) ? 0 : rr + 1;
+    sl3 = sl3 == 2 ? 0 : sl3 + 1;
+    if (t + 1 == R) break;
 
-    // 7. the releases for request t+1 (slot by slot, where some lane's head
-    // has finished); load request t+2
-    cur = nxt;
-    cu = nx_u;
-    cv = nx_v;
-    {
-      // (slots release independently, so all tests come first)
-      uint64_t any_done[M];
-#pragma unroll
-      for (int m = 0; m < M; ++m) any_done[m] = __ballot(s[m].h.t <= cur.now_eff);
-#pragma unroll
-      for (int m = 0; m < M; ++m)
-        if (any_done[m]) release_slot<kTok, kKv>(s[m], cur.now_eff, recr, R, dmy);
+    // 7. request t+1 (the next block moves in at a block boundary, and the
+    // block after it is loaded), then its releases
+    if (((t + 1) & 63) == 0) {
+      fb0 = fb1;
+      load_block(fb1, t + 1 + 64);
     }
-    release_more<M, kTok, kKv>(__any(head_min(s) <= cur.now_eff), s, cur.now_eff, recr, R, dmy);
+    cur = take((t + 1) & 63, t + 1);
     {
-      const int64_t g = base + min(t + 2, last);
-      nx_arr = a.arrival[g];
-      nx_p = a.plen[g];
-      nx_o = a.olen[g];
-      nx_oh = a.ohat[g];
-      nx_c = a.cls[g];
-      load_words(g, nx_u, nx_v);
+      bool done = false;
+#pragma unroll
+      for (int m = 0; m < M; ++m) done = done || s[m].h.t <= cur.now_eff;
+      if (__any(done)) {
+        static_for<M>([&](auto mc) __attribute__((always_inline)) {
+          constexpr int m = decltype(mc)::value;
+          if (__any(s[m].h.t <= cur.now_eff)) {
+            release_pop<kTok, kKv>(s[m], cur.now_eff);
+            if (__any(s[m].lq != 0)) {
+              load_refill<kTok>(s[m], recr, R, dmy);
+              pend |= 1u << m;
+            }
+          }
+        });
+        // a head still finished: more releases than the window holds
+        if (__builtin_expect(__any(head_min(s) <= cur.now_eff), 0)) {
+          release_more<M, kTok, kKv>(true, s, cur.now_eff, recr, R, dmy);
+          pend = (1u << M) - 1u;
+        }
+      }
     }
   }
-  const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u);
-  if (flag) atomicOr(a.flag, flag);
+  if (wave == 0) {
+    const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u);
+    if (flag && lane == 0) atomicOr(a.flag, flag);
+  }
 }
 
 template <int W, int M, int kMode>
