@@ -37,6 +37,13 @@ __device__ __forceinline__ T opaque(T x) {
   return x;
 }
 
+// Workgroup barrier for data exchanged through LDS: waits for this wave's
+// LDS operations, then s_barrier.  Unlike __syncthreads it does not wait for
+// the wave's global memory accesses (callers exchange nothing through global
+// memory between waves), and the memory clobber keeps the compiler from
+// moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Calls f(std::integral_constant<int, I>) for I = 0 .. N-1, so that code
 // acting on register-resident slots under a branch indexes them with
 // constants from the start (a loop index is constant only after unrolling,

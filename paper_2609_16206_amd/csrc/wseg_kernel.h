@@ -14,29 +14,50 @@
 // w + W * ((lane - LPW) * M + m), m < M.  Everything per request is uniform
 // over the workgroup.
 //
-// Argmin.  Each wave reduces both pools over its 64 lanes (DPP + readlane;
-// within a wave the lowest lane and slot hold the lowest index), then lane 0
-// of every wave folds its two winners into an LDS minimum of the packed key
-// (cost key << 32 | instance index), so equal costs keep the lowest index,
-// and writes their busy-until next to it.  After one barrier per step every
-// wave reads both minima and the two winners' busy-until, so all waves form
-// the same prefill and decode ends.  The LDS cells rotate over three step
-// slots: slot t % 3 is filled at step t, read after its barrier, and reset by
-// wave 0 after the barrier of step t + 1 (every wave has read it by then, and
-// none writes it again before the barrier of step t + 2).
+// Issue model.  With one wave per SIMD every instruction of the step, vector,
+// scalar, branch or LDS, takes an issue slot of about four cycles, and the
+// step is a chain of dependent work, so the kernel is written for the fewest
+// instructions per step rather than for the fewest vector ones.
 //
-// Per-step work is kept to one vector compare and one uniform branch per
-// phase where it is usually idle: the merge of refill loads runs only for
-// slots that issued one (a scalar mask), the releases only when some head of
-// the wave has finished, the slow path only when a head is still finished
-// after them, and the appends, whose FIFO position is the winner's queue
-// length read as a scalar, touch scratch only beyond the register window.
+// Requests.  The terms a step needs from its request (arrival, service
+// times, priced work and cache need per pool, sigma, the sampled
+// candidates) are derived once per block of 64 requests, lane k of every
+// wave working on request (block start + k), and left in LDS; a step reads
+// its request's record (96 bytes) from LDS one step ahead.  Admission (valid
+// lengths and class, arrival not before the last accepted one) is decided
+// for the whole block at once: a request is accepted if valid and its
+// arrival equals the running maximum of the valid arrivals so far, a prefix
+// maximum taken with DPP across the wave (the last accepted arrival is the
+// largest valid one before it, whether accepted or not).  The raw trace of a
+// block is loaded two blocks ahead.
 //
-// Requests and outcomes move in blocks of 64: lane k of every wave holds the
-// features of request (block start + k), loaded one block ahead with one
-// coalesced load per field, and a step reads its request with readlane;
-// wave 0's lane k keeps the outcome of step (block start + k) and the block
-// is written with one coalesced store per output array.
+// Argmin.  Each wave reduces both pools over its 64 lanes (DPP within rows,
+// row broadcasts across them; within a wave the lowest lane and slot hold
+// the lowest index), then lane 0 of every wave folds its two winners into an
+// LDS minimum of the packed key (cost key << 32 | instance index), so equal
+// costs keep the lowest index, and writes their busy-until next to it.
+// After one barrier per step (it orders LDS only: every global access of a
+// wave is to addresses no other wave touches) every wave reads both minima
+// and every wave's busy-until pair, and selects the winners', so all waves
+// form the same prefill and decode ends.
+// The LDS cells rotate over three step slots: slot t % 3 is filled at step
+// t, read after its barrier, and reset by wave 0 after the barrier of step
+// t + 1 (every wave has read it by then, and none writes it again before the
+// barrier of step t + 2).
+//
+// Sparse work.  The releases run only when some head of the wave has
+// finished (slot by slot, again while a head is still finished), a refill
+// from the successor records only where a queue is deeper than the window
+// (loaded and merged at once), and the appends, whose FIFO position is the
+// winner's queue length read as a scalar, touch scratch only beyond the
+// register window.  Each slot keeps
+// its queue term w_q * queue (and, pricing the ledger, its ledger backlog),
+// which change only with its queue, cached.
+//
+// Outcomes.  Each output array is kept by one wave (wave a keeps array a
+// with four or more waves; with two, each keeps two): lane k holds the
+// value of step (block start + k), and the block is written with one
+// coalesced store per array.
 #pragma once
 
 #include "seg_kernel.h"
@@ -53,9 +74,123 @@ __device__ __forceinline__ double rl_f64(double v, int lane) {
                           __builtin_amdgcn_readlane(__double2loint(v), lane));
 }
 
-__device__ __forceinline__ int64_t rl_i64(int64_t v, int lane) {
-  return (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int32_t)(v >> 32), lane) << 32) |
-                   (uint32_t)__builtin_amdgcn_readlane((int32_t)v, lane));
+// One instance of the wide kernel: the state the score reads, and the first
+// three positions of its FIFO (t = +inf beyond it).  A refill from the
+// successor records is loaded and merged at once (rare: only queues deeper
+// than the window need one), so no load is carried between steps.
+struct WSlot {
+  double busy;   // end of everything admitted so far
+  double kv;     // cache tokens in flight
+  double pend;   // ledger tokens in flight
+  int32_t q;     // requests in flight
+  int32_t tail;  // last admitted request
+  int32_t tail2; // the one admitted before it
+  Elem h, n, n2; // FIFO positions 0, 1, 2
+};
+
+__device__ __forceinline__ void init_wslot(WSlot& s) {
+  s.busy = s.kv = s.pend = 0.0;
+  s.q = 0;
+  s.tail = s.tail2 = -1;
+  s.h = s.n = s.n2 = none();
+}
+
+// The releases of one slot by `now_eff`, on the lanes whose head has
+// finished: up to two from the window, then the positions the shift left
+// empty refilled from the new head's record (refill_mask), loaded and
+// merged here where any lane of the wave needs one.
+template <bool kTok, bool kKv>
+__device__ __forceinline__ void wrelease(WSlot& x, double now_eff, const char* recr, int32_t R, int64_t dmy) {
+  const bool p1 = x.h.t <= now_eff;
+  const bool p2 = x.n.t <= now_eff;  // implies p1 (release times do not decrease)
+  x.q -= (p1 ? 1 : 0) + (p2 ? 1 : 0);
+  if constexpr (kKv) x.kv = x.kv - ((p1 ? (double)x.h.fp : 0.0) + (p2 ? (double)x.n.fp : 0.0));
+  if constexpr (kTok) x.pend = x.pend - ((p1 ? (double)x.h.pt : 0.0) + (p2 ? (double)x.n.pt : 0.0));
+  const Elem h1 = sel(p2, x.n2, sel(p1, x.n, x.h));
+  Elem n1 = sel(p1, x.n2, x.n);
+  n1.t = p2 ? kInf : n1.t;
+  x.h = h1;
+  x.n = n1;
+  x.n2.t = p1 ? kInf : x.n2.t;
+  const int32_t lq = opaque(refill_mask(p1, p2, x.q));
+  if (__any(lq != 0)) {
+    const int64_t g = sel_index(lq != 0, min(max(x.h.idx, 0), max(R - 1, 0)), dmy);
+    Slot tmp;
+    load_pair<kTok>(tmp, rec_at<kTok>(recr, g));
+    x.n = sel((lq & 1) != 0, tmp.l1, x.n);
+    x.n2 = sel((lq & 2) != 0, tmp.l2, x.n2);
+  }
+}
+
+template <int M>
+__device__ __forceinline__ double head_min_w(const WSlot (&s)[M]) {
+  double h = s[0].h.t;
+#pragma unroll
+  for (int m = 1; m < M; ++m) h = __builtin_fmin(h, s[m].h.t);
+  return h;
+}
+
+// A request as the lanes of one pool score it (32 bytes).
+struct alignas(16) PoolReq {
+  double now;       // arrival (ns) if the request is accepted, else -1
+  double need;      // cache tokens it needs on an instance of the pool
+  float work;       // priced work w_s * tokens * tau of the pool
+  float sg;         // sigma of its class
+  uint32_t c1, c2;  // the pool's sampled candidates
+};
+static_assert(sizeof(PoolReq) == 32, "two 16-byte words");
+
+// The rest of a request, read by the waves that serve, append or record it
+// (48 bytes).
+struct alignas(16) ServeReq {
+  double s_pre;        // prefill service
+  double xfer;         // KV transfer delay
+  double s_dec;        // decode service
+  int32_t p, po, oh;   // prompt, prompt + output, predicted output
+  int32_t pad;
+};
+static_assert(sizeof(ServeReq) == 48, "three 16-byte words");
+
+// One step of a wave-wide scan of doubles: x = max(x, x of the lane the DPP
+// control names); a lane without a source reads +0 (full row mask) or keeps
+// its value (partial row mask).
+template <int C, int RM>
+__device__ __forceinline__ double dpp_max_f64(double x) {
+  const int lo = __double2loint(x), hi = __double2hiint(x);
+  const int slo = __builtin_amdgcn_update_dpp(RM == 0xF ? 0 : lo, lo, C, RM, 0xF, RM == 0xF);
+  const int shi = __builtin_amdgcn_update_dpp(RM == 0xF ? 0 : hi, hi, C, RM, 0xF, RM == 0xF);
+  return __builtin_fmax(x, __hiloint2double(shi, slo));
+}
+
+// Inclusive prefix maximum over the wave of doubles >= -1 (lanes in order;
+// +0 enters as the maximum's floor): shifts of 1, 2, 4, 8 within each row of
+// 16 lanes, then the last lane of each row into the rows after it.
+__device__ __forceinline__ double wave_prefix_max(double x) {
+  x = dpp_max_f64<0x111, 0xF>(x);  // row_shr:1
+  x = dpp_max_f64<0x112, 0xF>(x);  // row_shr:2
+  x = dpp_max_f64<0x114, 0xF>(x);  // row_shr:4
+  x = dpp_max_f64<0x118, 0xF>(x);  // row_shr:8
+  x = dpp_max_f64<0x142, 0xA>(x);  // row_bcast:15 into rows 1 and 3
+  x = dpp_max_f64<0x143, 0xC>(x);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
+// Minimum over the wave of two values at once; lane 63 holds the results.
+__device__ __forceinline__ void wave_min2_to_63(uint32_t& v, uint32_t& w) {
+  v = min(v, dpp<0xB1>(v));
+  w = min(w, dpp<0xB1>(w));
+  v = min(v, dpp<0x4E>(v));
+  w = min(w, dpp<0x4E>(w));
+  v = min(v, dpp<0x141>(v));
+  w = min(w, dpp<0x141>(w));
+  v = min(v, dpp<0x140>(v));
+  w = min(w, dpp<0x140>(w));
+  // rows 1 and 3 take the last lane of the row before them, then rows 2 and
+  // 3 take lane 31 (the other rows keep their value)
+  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x142, 0xA, 0xF, false));
+  w = min(w, (uint32_t)__builtin_amdgcn_update_dpp((int)w, (int)w, 0x142, 0xA, 0xF, false));
+  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x143, 0xC, 0xF, false));
+  w = min(w, (uint32_t)__builtin_amdgcn_update_dpp((int)w, (int)w, 0x143, 0xC, 0xF, false));
 }
 
 template <int W, int M, int kMode>
@@ -82,13 +217,10 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   // instance m of this lane: wave + W * (lrel * M + m)
   const int32_t npool = isp ? P : D;
   const bool inpool = lane < LPW + LDW;
-  const float w_b = pt.w_b, w_s = pt.w_s, w_q = pt.w_q, rho = pt.rho;
+  const float w_b = pt.w_b, w_q = pt.w_q, rho = pt.rho;
   const float inv = isp ? pt.inv_cap_pre : pt.inv_cap_dec;
   const float tau = isp ? pt.tau_pre : pt.tau_dec;
   const float basec = isp ? pt.pre_base : 0.0f;  // proxy ledger: base per in-flight prefill
-  const double pre_base_ns = (double)pt.pre_base_ns, pre_tok_ns = (double)pt.pre_tok_ns;
-  const double dec_tok_ns = (double)pt.dec_tok_ns, xfer_tok_ns = (double)pt.xfer_tok_ns;
-  const float sigv = pt.sigma[lane & (kMaxClasses - 1)];  // lane k: sigma of class k mod 8
   char* const recb = isp ? a.rec[0] : a.rec[1];
   const uint32_t wave_id = (blockIdx.x * W + wave) & (kDummyRecords - 1);
   // the lane's plane at its replica's request 0; the wave's dummy record,
@@ -98,26 +230,39 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
 
   __shared__ unsigned long long best[3][2];  // per step slot: packed minimum of each pool
   __shared__ double wbusy[3][W][2];          // per step slot: each wave's winners' busy-until
+  // request records of the current and the next block: each pool's view,
+  // and the serving part
+  __shared__ PoolReq reqp[2][2][64];
+  __shared__ ServeReq reqv[2][64];
   if (threadIdx.x < 6) best[threadIdx.x >> 1][threadIdx.x & 1] = ~0ull;
-  __syncthreads();
 
-  Slot s[M];
-  bool ok[M];  // the slot holds an instance of the lane's pool
+  WSlot s[M];
+  bool ok[M];    // the slot holds an instance of the lane's pool
+  float wqq[M];  // w_q * (float)queue of each slot
+  float blv[M];  // ledger backlog of each slot (ledger modes)
 #pragma unroll
   for (int m = 0; m < M; ++m) {
-    init_slot(s[m]);
+    init_wslot(s[m]);
     ok[m] = inpool && wave + W * (lrel * M + m) < npool;
   }
+  // a slot's cached queue and ledger terms, after its queue or ledger changed
+  auto refresh = [&](int m) __attribute__((always_inline)) {
+    wqq[m] = w_q * (float)s[m].q;
+    if constexpr (kTok) blv[m] = tau * (float)s[m].pend + basec * (float)s[m].q;
+  };
+#pragma unroll
+  for (int m = 0; m < M; ++m) refresh(m);
 
-  // Features of a block of 64 requests, lane k holding request (block + k)
-  // (clamped into the replica).
-  struct Block {
+  // Raw trace of a block, lane k holding request (block start + k) (clamped
+  // into the replica; lanes past its end are rejected when the block's
+  // records are made).
+  struct Raw {
     int64_t arr;
     int32_t p, o, oh;
     uint32_t c;
     uint32_t w[4];  // candidate words (sampled modes)
   };
-  auto load_block = [&](Block& f, int32_t blk) __attribute__((always_inline)) {
+  auto load_raw = [&](Raw& f, int32_t blk) __attribute__((always_inline)) {
     const int64_t g = base + min(blk + lane, R - 1);
     f.arr = a.arrival[g];
     f.p = a.plen[g];
@@ -134,58 +279,80 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
       f.w[0] = f.w[1] = f.w[2] = f.w[3] = 0;
     }
   };
-  Block fb0, fb1;  // the current block and the next
-  load_block(fb0, 0);
-  load_block(fb1, 64);
-
-  double last_now = 0.0;  // latest accepted arrival (arrivals must not decrease)
-  float sg;               // sigma of the current request's class
-  uint32_t cu = 0, cv = 0;  // the lane's pool's candidate words of the current request
-  // Request k of the current block, checked against the replica (its
-  // features are uniform: read from lane k).
-  auto take = [&](int k, int32_t t) __attribute__((always_inline)) {
-    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.c, k);
-    sg = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int32_t, sigv), (int)(c & 7u)));
+  // The records of block `blk` from its raw trace, into buffer `buf`; `carry`
+  // is the largest valid arrival before the block (0 before the first).
+  const double pre_base_ns = (double)pt.pre_base_ns, pre_tok_ns = (double)pt.pre_tok_ns;
+  const double dec_tok_ns = (double)pt.dec_tok_ns, xfer_tok_ns = (double)pt.xfer_tok_ns;
+  const float w_s = pt.w_s, tau_pre = pt.tau_pre, tau_dec = pt.tau_dec;
+  const float sig_l = pt.sigma[lane & (kMaxClasses - 1)];  // lane k: sigma of class k mod 8
+  double carry = 0.0;
+  auto make_block = [&](const Raw& f, int32_t blk, int buf) __attribute__((always_inline)) {
+    const int32_t p = f.p, o = f.o, oh = f.oh;
+    const int32_t po = (int32_t)((uint32_t)p + (uint32_t)o), poh = (int32_t)((uint32_t)p + (uint32_t)oh);
+    const int32_t vm = min(min(min(p, o), min(oh, po)), min(min(poh, ncls - (int32_t)f.c), R - (blk + lane)));
+    const bool valid = opaque(vm) >= 1;
+    const double x = valid ? i64_to_f64(f.arr) : -1.0;
+    const double incl = __builtin_fmax(wave_prefix_max(x), carry);
+    carry = rl_f64(incl, 63);
+    const double now = (valid && x == incl) ? x : -1.0;
+    const float sg = __builtin_bit_cast(
+        float, __builtin_amdgcn_ds_bpermute((int)((f.c & (kMaxClasses - 1)) << 2), __builtin_bit_cast(int, sig_l)));
+    uint32_t c[4] = {0, 0, 0, 0};
     if constexpr (kSamp) {
-      const uint32_t w0 = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.w[0], k);
-      const uint32_t w1 = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.w[1], k);
-      const uint32_t w2 = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.w[2], k);
-      const uint32_t w3 = (uint32_t)__builtin_amdgcn_readlane((int32_t)fb0.w[3], k);
-      cu = isp ? w0 : w2;
-      cv = isp ? w1 : w3;
+      sample_pair(f.w[0], f.w[1], (uint32_t)P, c[0], c[1]);
+      sample_pair(f.w[2], f.w[3], (uint32_t)D, c[2], c[3]);
     }
-    return admit_check(R - t, ncls, rl_i64(fb0.arr, k), __builtin_amdgcn_readlane(fb0.p, k),
-                       __builtin_amdgcn_readlane(fb0.o, k), __builtin_amdgcn_readlane(fb0.oh, k), c, last_now);
+    reqp[buf][0][lane] = PoolReq{now, (double)p, w_s * (float)p * tau_pre, sg, c[0], c[1]};
+    reqp[buf][1][lane] = PoolReq{now, (double)poh, w_s * (float)oh * tau_dec, sg, c[2], c[3]};
+    reqv[buf][lane] = ServeReq{__builtin_fma((double)p, pre_tok_ns, pre_base_ns), (double)p * xfer_tok_ns,
+                               (double)(o - 1) * dec_tok_ns, p, po, oh, 0};
   };
-  Req cur = take(0, 0);
 
-  // outcomes of the current block (wave 0, lane k: step block start + k)
-  int32_t b_ip = -1, b_id = -1;
-  int64_t b_tt = -1, b_sp = -1;
-  int32_t rr = 0;      // round robin: t mod (size of this lane's pool)
-  double tmax = 0.0;   // latest decode end (time-range check)
-  bool rej = false;    // a request was rejected
-  uint32_t pend = 0;   // slots whose refill load is in flight (bit m)
-  int sl3 = 0;         // step slot t % 3 of the LDS cells
+  Raw raw;
+  load_raw(raw, 0);
+  make_block(raw, 0, 0);
+  load_raw(raw, 64);
+  __syncthreads();
+  const int pl = isp ? 0 : 1;  // the lane's pool
+  PoolReq rq = reqp[0][pl][0];  // the current request as the lane's pool scores it
+
+  // outcomes of the current block kept by this wave (lane k: step block
+  // start + k): an int32 array (0 i_pre, 1 i_dec) and an int64 array (0
+  // ttft, 1 span), or none (-1)
+  const int oi = W == 2 ? wave : (wave < 2 ? wave : -1);
+  const int ol = W == 2 ? wave : (wave == 2 ? 0 : (wave == 3 ? 1 : -1));
+  int32_t b32 = -1;
+  int64_t b64 = -1;
+  int32_t rr = 0;     // round robin: t mod (size of this lane's pool)
+  double tmax = 0.0;  // latest decode end (time-range check)
+  bool rej = false;   // a request was rejected
+  int sl3 = 0;        // step slot t % 3 of the LDS cells
 
   for (int32_t t = 0; t < R; ++t) {
-    const int32_t p = cur.p, o = cur.o, oh = cur.oh, po = cur.po, poh = cur.poh;
-    const double now = cur.now;
-    const bool go = cur.go;
+    // at a block boundary: the records of the next block, and the raw trace
+    // of the one after it
+    if ((t & 63) == 0) {
+      make_block(raw, t + 64, ((t >> 6) + 1) & 1);
+      load_raw(raw, t + 128);
+    }
+    const int buf = (t >> 6) & 1, k = t & 63;
+    const double now = rq.now;
+    const bool go = now >= 0.0;
 
     // 1. score this lane's instances
-    const int32_t cnt = isp ? p : oh;
-    const float work = w_s * (float)cnt * tau;
-    const double need = (double)(isp ? p : poh);
-    const bool long_req = oh >= len_thr;  // length threshold: the upper part
+    const float work = rq.work;
+    const double need = rq.need;
+    const float sg = rq.sg;
+    bool long_req = false;  // length threshold: the request uses the upper part
+    if constexpr (kMode == kModeBase)
+      if (thr) long_req = reqv[buf][k].oh >= len_thr;
     uint32_t bkey = 0xffffffffu;
     int32_t bm = 0;
     double bbusy = s[0].busy;
-    uint32_t c1 = 0, c2 = 0;  // the pool's sampled candidates
-    if constexpr (kSamp) sample_pair(cu, cv, (uint32_t)npool, c1, c2);
+    const uint32_t c1 = rq.c1, c2 = rq.c2;
 #pragma unroll
     for (int m = 0; m < M; ++m) {
-      const Slot& x = s[m];
+      const WSlot& x = s[m];
       uint32_t key;
       if constexpr (kMode == kModeBase) {
         // round robin; least loaded; or least loaded within the decode
@@ -199,11 +366,11 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
         if constexpr (!kTok)
           bl = (float)__builtin_fmax(x.busy - now, 0.0) * 1e-9f;
         else
-          bl = tau * (float)x.pend + basec * (float)x.q;
+          bl = blv[m];
         const float press = (float)(x.kv + need) * inv;
         const float load = w_b * bl * sg;
         const float size = work * (1.0f + rho * press) * sg;
-        const float cost = load + size + w_q * (float)x.q;
+        const float cost = load + size + wqq[m];
         key = cost != cost ? 0x7fc00000u : __float_as_uint(cost);
       }
       if constexpr (kSamp) {
@@ -226,79 +393,80 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     {
       uint32_t kp = isp ? bkey : 0xffffffffu, kd = isp ? 0xffffffffu : bkey;
       const uint32_t kp0 = kp, kd0 = kd;
-      seg_min2<64>(kp, kd, lane);
-      const int32_t wp = seg_first<64>(kp0 == kp, lane) & 63;  // the wave's winning lanes
-      const int32_t wd = seg_first<64>(kd0 == kd, lane) & 63;
+      wave_min2_to_63(kp, kd);
+      const uint32_t mkp = (uint32_t)__builtin_amdgcn_readlane((int)kp, 63);
+      const uint32_t mkd = (uint32_t)__builtin_amdgcn_readlane((int)kd, 63);
+      // the wave's winning lanes: the lowest lane holding each minimum
+      const int32_t wp = (__ffsll((unsigned long long)__ballot(kp0 == mkp)) - 1) & 63;
+      const int32_t wd = (__ffsll((unsigned long long)__ballot(kd0 == mkd)) - 1) & 63;
       const int32_t mpw = __builtin_amdgcn_readlane(bm, wp);
       const int32_t mdw = __builtin_amdgcn_readlane(bm, wd);
       const double bpw = rl_f64(bbusy, wp), bdw = rl_f64(bbusy, wd);
       const uint32_t ipw = (uint32_t)(wave + W * (wp * M + mpw));
       const uint32_t idw = (uint32_t)(wave + W * ((wd - LPW) * M + mdw));
       if (lane == 0) {
-        atomicMin(&best[sl3][0], ((unsigned long long)kp << 32) | ipw);
-        atomicMin(&best[sl3][1], ((unsigned long long)kd << 32) | idw);
+        atomicMin(&best[sl3][0], ((unsigned long long)mkp << 32) | ipw);
+        atomicMin(&best[sl3][1], ((unsigned long long)mkd << 32) | idw);
         wbusy[sl3][wave][0] = bpw;
         wbusy[sl3][wave][1] = bdw;
       }
     }
-    __syncthreads();
+    lds_barrier();
     const int32_t ip = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)best[sl3][0]);
     const int32_t id = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)best[sl3][1]);
-    double busy_ip = wbusy[sl3][0][0], busy_id = wbusy[sl3][0][1];
-#pragma unroll
-    for (int w = 1; w < W; ++w) {
-      busy_ip = (ip & (W - 1)) == w ? wbusy[sl3][w][0] : busy_ip;
-      busy_id = (id & (W - 1)) == w ? wbusy[sl3][w][1] : busy_id;
+    // the waves that need them: the winners' and the ones that record the
+    // ends (the time-range check rides with the decode span)
+    const bool win_p = wave == (ip & (W - 1)), win_d = wave == (id & (W - 1));
+    double pf_end = 0.0, de = 0.0;
+    int32_t sp_p = 0, sp_po = 0, sp_oh = 0;
+    if (go && (win_p || win_d || ol >= 0)) {
+      const double busy_ip = wbusy[sl3][ip & (W - 1)][0];
+      const double busy_id = wbusy[sl3][id & (W - 1)][1];
+      const ServeReq sv = reqv[buf][k];
+      // 3. serve: prefill, KV transfer, decode (exact integers in doubles)
+      pf_end = __builtin_fmax(now, busy_ip) + sv.s_pre;
+      const double kv_at = pf_end + sv.xfer;
+      de = __builtin_fmax(kv_at, busy_id) + sv.s_dec;
+      sp_p = sv.p;
+      sp_po = sv.po;
+      sp_oh = sv.oh;
     }
     // the cells of step t - 1 are free again (every wave has read them)
     const int sl_prev = sl3 == 0 ? 2 : sl3 - 1;
     if (wave == 0 && lane < 2) best[sl_prev][lane] = ~0ull;
-
-    // 3. serve (uniform): prefill, KV transfer, decode (exact integers in
-    // doubles)
-    const double s_pre = __builtin_fma((double)p, pre_tok_ns, pre_base_ns);
-    const double pf_end = __builtin_fmax(now, busy_ip) + s_pre;
-    const double kv_at = pf_end + (double)p * xfer_tok_ns;
-    const double de = __builtin_fmax(kv_at, busy_id) + (double)(o - 1) * dec_tok_ns;
-
-    // 4. refill loads of request t's releases, where any were issued
-    if (pend) {
-      static_for<M>([&](auto mc) __attribute__((always_inline)) {
-        if (pend & (1u << decltype(mc)::value)) merge_pending(s[decltype(mc)::value]);
-      });
-      pend = 0;
-    }
+    // the next request's record (read a step ahead)
+    const PoolReq rn = reqp[((t + 1) >> 6) & 1][pl][(t + 1) & 63];
 
     // 5. append the request to the winning slot of each pool (uniform
     // branches: the winner's wave and slot, then its FIFO position)
     if (go) {
-      auto append = [&](int32_t win, int32_t lane_off, double end, int32_t fp, int32_t tk) __attribute__((always_inline)) {
+      auto append = [&](int32_t win, int32_t lane_off, double end, int32_t fp, int32_t tk)
+                        __attribute__((always_inline)) {
         const int32_t q = win >> kLogW;       // position within the wave
         const int32_t lw = lane_off + q / M;  // lane
-        const int32_t mw = q - (q / M) * M;  // slot
+        const int32_t mw = q - (q / M) * M;   // slot
         const bool own = lane == lw;
         const Elem z{end, t, fp, tk};
         static_for<M>([&](auto mc) __attribute__((always_inline)) {
           constexpr int m = decltype(mc)::value;
           if (m != mw) return;
-          Slot& x = s[m];
+          WSlot& x = s[m];
           const int32_t w = __builtin_amdgcn_readlane(x.q, lw);  // z's FIFO position
-          if (w == 0) {
-            x.h = sel(own, z, x.h);
-          } else if (w == 1) {
-            x.n = sel(own, z, x.n);
-          } else if (w == 2) {
-            x.n2 = sel(own, z, x.n2);
-          } else if (own) {
+          x.h = sel(own && w == 0, z, x.h);
+          x.n = sel(own && w == 1, z, x.n);
+          x.n2 = sel(own && w == 2, z, x.n2);
+          if (w >= 3) {
             // beyond the window: z is the first successor of the tail and
             // the second of the request before it
-            char* const r1 = rec_at<kTok>(recr, x.tail);
-            char* const r2 = rec_at<kTok>(recr, x.tail2);
-            *reinterpret_cast<Entry*>(r1) = Entry{end, t, fp};
-            *reinterpret_cast<Entry*>(r2 + 16) = Entry{end, t, fp};
-            if constexpr (kTok) {
-              *reinterpret_cast<int32_t*>(r1 + kRecTok) = tk;
-              *reinterpret_cast<int32_t*>(r2 + kRecTok + 4) = tk;
+            if (own) {
+              char* const r1 = rec_at<kTok>(recr, x.tail);
+              char* const r2 = rec_at<kTok>(recr, x.tail2);
+              *reinterpret_cast<Entry*>(r1) = Entry{end, t, fp};
+              *reinterpret_cast<Entry*>(r2 + 16) = Entry{end, t, fp};
+              if constexpr (kTok) {
+                *reinterpret_cast<int32_t*>(r1 + kRecTok) = tk;
+                *reinterpret_cast<int32_t*>(r2 + kRecTok + 4) = tk;
+              }
             }
           }
           const int32_t tl_old = x.tail;
@@ -308,70 +476,66 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           if constexpr (kKv) x.kv = x.kv + (own ? (double)fp : 0.0);
           if constexpr (kTok) x.pend = x.pend + (own ? (double)tk : 0.0);
           x.busy = own ? end : x.busy;
+          refresh(m);
         });
       };
-      if (wave == (ip & (W - 1))) append(ip, 0, pf_end, p, p);
-      if (wave == (id & (W - 1))) append(id, LPW, de, po, oh);
+      if (win_p) append(ip, 0, pf_end, sp_p, sp_p);
+      if (win_d) append(id, LPW, de, sp_po, sp_oh);
     }
 
-    // 6. the outcome, kept by wave 0's lane t mod 64 until its block is
-    // written
-    if (wave == 0) {
+    // 6. the outcome: each array kept by its wave, written per block of 64
+    {
       const bool keep = lane == (t & 63);
-      b_ip = keep ? (go ? ip : -1) : b_ip;
-      b_id = keep ? (go ? id : -1) : b_id;
-      b_tt = keep ? (go ? f64_to_i64(pf_end - now) : -1) : b_tt;
-      b_sp = keep ? (go ? f64_to_i64(de - pf_end) : -1) : b_sp;
-      tmax = go ? __builtin_fmax(tmax, de) : tmax;
-      rej = rej || !go;
+      if (oi >= 0) b32 = keep ? (go ? (oi == 0 ? ip : id) : -1) : b32;
+      if (ol >= 0) b64 = keep ? (go ? f64_to_i64(ol == 0 ? pf_end - now : de - pf_end) : -1) : b64;
       if ((t & 63) == 63 || t == R - 1) {
         const int32_t tl = (t & ~63) + lane;
         if (tl <= t) {
           const int64_t gi = base + tl;
-          a.i_pre[gi] = b_ip;
-          a.i_dec[gi] = b_id;
-          a.ttft[gi] = b_tt;
-          a.span[gi] = b_sp;
+          if (oi >= 0) (oi == 0 ? a.i_pre : a.i_dec)[gi] = b32;
+          if (ol >= 0) (ol == 0 ? a.ttft : a.span)[gi] = b64;
         }
       }
     }
+    if (ol == 1) tmax = go ? __builtin_fmax(tmax, de) : tmax;
+    rej = rej || !go;
     if constexpr (kMode == kModeBase) rr = (rr + 1 == npool) ? 0 : rr + 1;
     sl3 = sl3 == 2 ? 0 : sl3 + 1;
-    if (t + 1 == R) break;
+    rq = rn;
 
-    // 7. request t+1 (the next block moves in at a block boundary, and the
-    // block after it is loaded), then its releases
-    if (((t + 1) & 63) == 0) {
-      fb0 = fb1;
-      load_block(fb1, t + 1 + 64);
-    }
-    cur = take((t + 1) & 63, t + 1);
+    // 7. the releases for request t+1: slot by slot where some lane's head
+    // has finished, again while a head is still finished (more releases
+    // than the window holds)
     {
+      const double now_eff = rq.now;
       bool done = false;
 #pragma unroll
-      for (int m = 0; m < M; ++m) done = done || s[m].h.t <= cur.now_eff;
+      for (int m = 0; m < M; ++m) done = done || s[m].h.t <= now_eff;
       if (__any(done)) {
         static_for<M>([&](auto mc) __attribute__((always_inline)) {
           constexpr int m = decltype(mc)::value;
-          if (__any(s[m].h.t <= cur.now_eff)) {
-            release_pop<kTok, kKv>(s[m], cur.now_eff);
-            if (__any(s[m].lq != 0)) {
-              load_refill<kTok>(s[m], recr, R, dmy);
-              pend |= 1u << m;
-            }
+          if (__any(s[m].h.t <= now_eff)) {
+            wrelease<kTok, kKv>(s[m], now_eff, recr, R, dmy);
+            refresh(m);
           }
         });
-        // a head still finished: more releases than the window holds
-        if (__builtin_expect(__any(head_min(s) <= cur.now_eff), 0)) {
-          release_more<M, kTok, kKv>(true, s, cur.now_eff, recr, R, dmy);
-          pend = (1u << M) - 1u;
+        if (__builtin_expect(__any(head_min_w(s) <= now_eff), 0)) {
+          do {
+            static_for<M>([&](auto mc) __attribute__((always_inline)) {
+              constexpr int m = decltype(mc)::value;
+              if (__any(s[m].h.t <= now_eff)) {
+                wrelease<kTok, kKv>(s[m], now_eff, recr, R, dmy);
+                refresh(m);
+              }
+            });
+          } while (__any(head_min_w(s) <= now_eff));
         }
       }
     }
   }
-  if (wave == 0) {
+  if (lane == 0 && (ol == 1 || wave == 0)) {
     const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u);
-    if (flag && lane == 0) atomicOr(a.flag, flag);
+    if (flag) atomicOr(a.flag, flag);
   }
 }
 
@@ -385,7 +549,7 @@ hipError_t launch_wseg(const SimArgs& a, hipStream_t stream) {
 // The workgroup widths (waves) and lane depths compiled for every mode, in
 // order of preference: at most one wave per SIMD of a compute unit first
 // (then fewer instances per lane), then eight waves.
-#define RT_WSEG_FOR_EACH(X) X(2, 2) X(4, 2) X(2, 3) X(4, 3) X(4, 5) X(8, 2) X(8, 3) X(8, 5)
+#define RT_WSEG_FOR_EACH(X) X(2, 2) X(4, 2) X(2, 3) X(4, 3) X(8, 3) X(4, 5) X(8, 2) X(8, 5)
 
 template <int kMode>
 hipError_t launch_wide_mode(int W, int M, const SimArgs& a, hipStream_t stream);
