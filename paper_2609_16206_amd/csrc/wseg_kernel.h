@@ -14,10 +14,13 @@
 // w + W * ((lane - LPW) * M + m), m < M.  Everything per request is uniform
 // over the workgroup.
 //
-// Issue model.  With one wave per SIMD every instruction of the step, vector,
-// scalar, branch or LDS, takes an issue slot of about four cycles, and the
-// step is a chain of dependent work, so the kernel is written for the fewest
-// instructions per step rather than for the fewest vector ones.
+// Issue model.  A wave issues about one instruction every four cycles,
+// vector, scalar, branch or LDS alike, and the step is a chain of dependent
+// work ending in a barrier, so the kernel is written for the fewest
+// instructions per step rather than for the fewest vector ones; two waves
+// per SIMD (eight per workgroup) let one wave's waits overlap the other's
+// issue, which pays more than the extra lanes cost (the large pool's 1,152
+// instances run at three per lane on eight waves).
 //
 // Requests.  The terms a step needs from its request (arrival, service
 // times, priced work and cache need per pool, sigma, the sampled
@@ -38,8 +41,8 @@
 // costs keep the lowest index, and writes their busy-until next to it.
 // After one barrier per step (it orders LDS only: every global access of a
 // wave is to addresses no other wave touches) every wave reads both minima
-// and every wave's busy-until pair, and selects the winners', so all waves
-// form the same prefill and decode ends.
+// and then the two winners' busy-until, so all waves form the same prefill
+// and decode ends.
 // The LDS cells rotate over three step slots: slot t % 3 is filled at step
 // t, read after its barrier, and reset by wave 0 after the barrier of step
 // t + 1 (every wave has read it by then, and none writes it again before the
@@ -50,9 +53,10 @@
 // from the successor records only where a queue is deeper than the window
 // (loaded and merged at once), and the appends, whose FIFO position is the
 // winner's queue length read as a scalar, touch scratch only beyond the
-// register window.  Each slot keeps
-// its queue term w_q * queue (and, pricing the ledger, its ledger backlog),
-// which change only with its queue, cached.
+// register window.  Each slot keeps its queue term w_q * queue (and,
+// pricing the ledger, its ledger backlog), which change only with its
+// queue, cached.  The step loop is unrolled by two, so that the request
+// records alternate between two register sets.
 //
 // Outcomes.  Each output array is kept by one wave (wave a keeps array a
 // with four or more waves; with two, each keeps two): lane k holds the
@@ -130,26 +134,20 @@ __device__ __forceinline__ double head_min_w(const WSlot (&s)[M]) {
   return h;
 }
 
-// A request as the lanes of one pool score it (32 bytes).
-struct alignas(16) PoolReq {
-  double now;       // arrival (ns) if the request is accepted, else -1
-  double need;      // cache tokens it needs on an instance of the pool
-  float work;       // priced work w_s * tokens * tau of the pool
-  float sg;         // sigma of its class
-  uint32_t c1, c2;  // the pool's sampled candidates
+// A request as a step of the wide kernel reads it (96 bytes).
+struct alignas(16) WReq {
+  double now;             // arrival (ns) if the request is accepted, else -1
+  double s_pre;           // prefill service
+  double xfer;            // KV transfer delay
+  double s_dec;           // decode service
+  double need_p, need_d;  // cache tokens it needs on a prefill / decode instance
+  float work_p, work_d;   // priced work w_s * tokens * tau of each pool
+  float sg;               // sigma of its class
+  int32_t p, po, oh;      // prompt, prompt + output, predicted output
+  uint32_t cand[4];       // sampled candidates: prefill c1, c2, decode c1, c2
+  int32_t pad[2];
 };
-static_assert(sizeof(PoolReq) == 32, "two 16-byte words");
-
-// The rest of a request, read by the waves that serve, append or record it
-// (48 bytes).
-struct alignas(16) ServeReq {
-  double s_pre;        // prefill service
-  double xfer;         // KV transfer delay
-  double s_dec;        // decode service
-  int32_t p, po, oh;   // prompt, prompt + output, predicted output
-  int32_t pad;
-};
-static_assert(sizeof(ServeReq) == 48, "three 16-byte words");
+static_assert(sizeof(WReq) == 96, "six 16-byte words");
 
 // One step of a wave-wide scan of doubles: x = max(x, x of the lane the DPP
 // control names); a lane without a source reads +0 (full row mask) or keeps
@@ -230,10 +228,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
 
   __shared__ unsigned long long best[3][2];  // per step slot: packed minimum of each pool
   __shared__ double wbusy[3][W][2];          // per step slot: each wave's winners' busy-until
-  // request records of the current and the next block: each pool's view,
-  // and the serving part
-  __shared__ PoolReq reqp[2][2][64];
-  __shared__ ServeReq reqv[2][64];
+  __shared__ WReq reqs[2][64];               // request records of the current and the next block
   if (threadIdx.x < 6) best[threadIdx.x >> 1][threadIdx.x & 1] = ~0ull;
 
   WSlot s[M];
@@ -279,7 +274,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
       f.w[0] = f.w[1] = f.w[2] = f.w[3] = 0;
     }
   };
-  // The records of block `blk` from its raw trace, into buffer `buf`; `carry`
+  // The records of block `blk` from its raw trace, into reqs[buf]; `carry`
   // is the largest valid arrival before the block (0 before the first).
   const double pre_base_ns = (double)pt.pre_base_ns, pre_tok_ns = (double)pt.pre_tok_ns;
   const double dec_tok_ns = (double)pt.dec_tok_ns, xfer_tok_ns = (double)pt.xfer_tok_ns;
@@ -294,18 +289,28 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     const double x = valid ? i64_to_f64(f.arr) : -1.0;
     const double incl = __builtin_fmax(wave_prefix_max(x), carry);
     carry = rl_f64(incl, 63);
-    const double now = (valid && x == incl) ? x : -1.0;
-    const float sg = __builtin_bit_cast(
+    WReq r;
+    r.now = (valid && x == incl) ? x : -1.0;
+    r.s_pre = __builtin_fma((double)p, pre_tok_ns, pre_base_ns);
+    r.xfer = (double)p * xfer_tok_ns;
+    r.s_dec = (double)(o - 1) * dec_tok_ns;
+    r.need_p = (double)p;
+    r.need_d = (double)poh;
+    r.work_p = w_s * (float)p * tau_pre;
+    r.work_d = w_s * (float)oh * tau_dec;
+    r.sg = __builtin_bit_cast(
         float, __builtin_amdgcn_ds_bpermute((int)((f.c & (kMaxClasses - 1)) << 2), __builtin_bit_cast(int, sig_l)));
-    uint32_t c[4] = {0, 0, 0, 0};
+    r.p = p;
+    r.po = po;
+    r.oh = oh;
     if constexpr (kSamp) {
-      sample_pair(f.w[0], f.w[1], (uint32_t)P, c[0], c[1]);
-      sample_pair(f.w[2], f.w[3], (uint32_t)D, c[2], c[3]);
+      sample_pair(f.w[0], f.w[1], (uint32_t)P, r.cand[0], r.cand[1]);
+      sample_pair(f.w[2], f.w[3], (uint32_t)D, r.cand[2], r.cand[3]);
+    } else {
+      r.cand[0] = r.cand[1] = r.cand[2] = r.cand[3] = 0;
     }
-    reqp[buf][0][lane] = PoolReq{now, (double)p, w_s * (float)p * tau_pre, sg, c[0], c[1]};
-    reqp[buf][1][lane] = PoolReq{now, (double)poh, w_s * (float)oh * tau_dec, sg, c[2], c[3]};
-    reqv[buf][lane] = ServeReq{__builtin_fma((double)p, pre_tok_ns, pre_base_ns), (double)p * xfer_tok_ns,
-                               (double)(o - 1) * dec_tok_ns, p, po, oh, 0};
+    r.pad[0] = r.pad[1] = 0;
+    reqs[buf][lane] = r;
   };
 
   Raw raw;
@@ -313,8 +318,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   make_block(raw, 0, 0);
   load_raw(raw, 64);
   __syncthreads();
-  const int pl = isp ? 0 : 1;  // the lane's pool
-  PoolReq rq = reqp[0][pl][0];  // the current request as the lane's pool scores it
+  WReq rq = reqs[0][0];  // the current request's record
 
   // outcomes of the current block kept by this wave (lane k: step block
   // start + k): an int32 array (0 i_pre, 1 i_dec) and an int64 array (0
@@ -328,28 +332,26 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   bool rej = false;   // a request was rejected
   int sl3 = 0;        // step slot t % 3 of the LDS cells
 
-  for (int32_t t = 0; t < R; ++t) {
+  // one step; request t's record is rq, request t+1's is read into rn
+  auto step = [&](const int32_t t, WReq& rq, WReq& rn) __attribute__((always_inline)) {
     // at a block boundary: the records of the next block, and the raw trace
     // of the one after it
     if ((t & 63) == 0) {
       make_block(raw, t + 64, ((t >> 6) + 1) & 1);
       load_raw(raw, t + 128);
     }
-    const int buf = (t >> 6) & 1, k = t & 63;
     const double now = rq.now;
     const bool go = now >= 0.0;
 
     // 1. score this lane's instances
-    const float work = rq.work;
-    const double need = rq.need;
+    const float work = isp ? rq.work_p : rq.work_d;
+    const double need = isp ? rq.need_p : rq.need_d;
     const float sg = rq.sg;
-    bool long_req = false;  // length threshold: the request uses the upper part
-    if constexpr (kMode == kModeBase)
-      if (thr) long_req = reqv[buf][k].oh >= len_thr;
+    const bool long_req = rq.oh >= len_thr;  // length threshold: the upper part
     uint32_t bkey = 0xffffffffu;
     int32_t bm = 0;
     double bbusy = s[0].busy;
-    const uint32_t c1 = rq.c1, c2 = rq.c2;
+    const uint32_t c1 = isp ? rq.cand[0] : rq.cand[2], c2 = isp ? rq.cand[1] : rq.cand[3];
 #pragma unroll
     for (int m = 0; m < M; ++m) {
       const WSlot& x = s[m];
@@ -414,28 +416,19 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     lds_barrier();
     const int32_t ip = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)best[sl3][0]);
     const int32_t id = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)best[sl3][1]);
-    // the waves that need them: the winners' and the ones that record the
-    // ends (the time-range check rides with the decode span)
-    const bool win_p = wave == (ip & (W - 1)), win_d = wave == (id & (W - 1));
-    double pf_end = 0.0, de = 0.0;
-    int32_t sp_p = 0, sp_po = 0, sp_oh = 0;
-    if (go && (win_p || win_d || ol >= 0)) {
-      const double busy_ip = wbusy[sl3][ip & (W - 1)][0];
-      const double busy_id = wbusy[sl3][id & (W - 1)][1];
-      const ServeReq sv = reqv[buf][k];
-      // 3. serve: prefill, KV transfer, decode (exact integers in doubles)
-      pf_end = __builtin_fmax(now, busy_ip) + sv.s_pre;
-      const double kv_at = pf_end + sv.xfer;
-      de = __builtin_fmax(kv_at, busy_id) + sv.s_dec;
-      sp_p = sv.p;
-      sp_po = sv.po;
-      sp_oh = sv.oh;
-    }
+    const double busy_ip = wbusy[sl3][ip & (W - 1)][0];
+    const double busy_id = wbusy[sl3][id & (W - 1)][1];
     // the cells of step t - 1 are free again (every wave has read them)
     const int sl_prev = sl3 == 0 ? 2 : sl3 - 1;
     if (wave == 0 && lane < 2) best[sl_prev][lane] = ~0ull;
     // the next request's record (read a step ahead)
-    const PoolReq rn = reqp[((t + 1) >> 6) & 1][pl][(t + 1) & 63];
+    rn = reqs[((t + 1) >> 6) & 1][(t + 1) & 63];
+
+    // 3. serve (uniform): prefill, KV transfer, decode (exact integers in
+    // doubles)
+    const double pf_end = __builtin_fmax(now, busy_ip) + rq.s_pre;
+    const double kv_at = pf_end + rq.xfer;
+    const double de = __builtin_fmax(kv_at, busy_id) + rq.s_dec;
 
     // 5. append the request to the winning slot of each pool (uniform
     // branches: the winner's wave and slot, then its FIFO position)
@@ -479,8 +472,8 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           refresh(m);
         });
       };
-      if (win_p) append(ip, 0, pf_end, sp_p, sp_p);
-      if (win_d) append(id, LPW, de, sp_po, sp_oh);
+      if (wave == (ip & (W - 1))) append(ip, 0, pf_end, rq.p, rq.p);
+      if (wave == (id & (W - 1))) append(id, LPW, de, rq.po, rq.oh);
     }
 
     // 6. the outcome: each array kept by its wave, written per block of 64
@@ -497,17 +490,16 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
         }
       }
     }
-    if (ol == 1) tmax = go ? __builtin_fmax(tmax, de) : tmax;
+    tmax = go ? __builtin_fmax(tmax, de) : tmax;
     rej = rej || !go;
     if constexpr (kMode == kModeBase) rr = (rr + 1 == npool) ? 0 : rr + 1;
     sl3 = sl3 == 2 ? 0 : sl3 + 1;
-    rq = rn;
 
     // 7. the releases for request t+1: slot by slot where some lane's head
     // has finished, again while a head is still finished (more releases
     // than the window holds)
     {
-      const double now_eff = rq.now;
+      const double now_eff = rn.now;
       bool done = false;
 #pragma unroll
       for (int m = 0; m < M; ++m) done = done || s[m].h.t <= now_eff;
@@ -532,8 +524,15 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
         }
       }
     }
+  };
+  // two steps per trip, so that the records alternate between two register
+  // sets instead of being copied
+  WReq rb;
+  for (int32_t t = 0; t < R; t += 2) {
+    step(t, rq, rb);
+    if (t + 1 < R) step(t + 1, rb, rq);
   }
-  if (lane == 0 && (ol == 1 || wave == 0)) {
+  if (wave == 0 && lane == 0) {
     const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u);
     if (flag) atomicOr(a.flag, flag);
   }
