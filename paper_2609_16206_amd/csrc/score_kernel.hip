@@ -8,10 +8,11 @@
 // thread scores kReq requests against every instance, reading each LDS entry
 // once for all of its requests.  VALU-bound.
 //
-// Per-request snapshot (inst_stride >= n_inst): a segment of S lanes per
-// request walks the request's row with unit stride across lanes (coalesced),
-// keeps a lane-local best, and reduces (key, index) over the segment.
-// HBM-bound.
+// Per-request snapshot (inst_stride >= n_inst): rows of at most 64 instances
+// laid out for 16-byte loads take 16 lanes per request, four instances per
+// lane; any other shape takes a segment of S lanes per request that walks the
+// request's row with unit stride across lanes (coalesced), keeps a
+// lane-local best, and reduces (key, index) over the segment.  HBM-bound.
 #include "rt_internal.h"
 
 namespace rt {
@@ -160,6 +161,87 @@ __global__ void __launch_bounds__(kBlock) score_rows_kernel(ScoreArgs a) {
   }
 }
 
+// Per-request rows of at most 64 instances, n_inst and the stride multiples
+// of 4 and the snapshot arrays 16-byte aligned: 16 lanes per request, four
+// consecutive instances per lane (one 16-byte load per array), four
+// requests per wave and kRowGroups groups of four per wave, every load of a
+// wave issued before its first cost.  Within a lane the four costs are taken
+// in index order (the first of equal keys stays); the 16 lanes of a request
+// reduce the key, then the lowest index holding it, with DPP within their
+// row.
+constexpr int kRowGroups = 4;
+
+__device__ __forceinline__ uint32_t row_min(uint32_t v) {
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, true));   // quad_perm xor 1
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, true));   // quad_perm xor 2
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, true));  // row_half_mirror
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xF, 0xF, true));  // row_mirror
+  return v;
+}
+
+__global__ void __launch_bounds__(kBlock) score_rows16_kernel(ScoreArgs a) {
+  constexpr int G = kRowGroups;
+  const int lane = threadIdx.x & 63;
+  const int rq = lane >> 4, ql = lane & 15;
+  const int64_t wave = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  const int64_t first = wave * 4 * G;
+  const int j0 = 4 * ql;  // this lane's first instance
+  const bool lane_in = j0 < a.n_inst;
+  float4 b4[G];
+  int4 q4[G], k4[G];
+  int32_t p[G], oh[G];
+  uint32_t c[G];
+  bool live[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int64_t i = first + 4 * g + rq;
+    live[g] = i < a.n_req;
+    const int64_t ii = live[g] ? i : 0;
+    p[g] = a.plen[ii];
+    oh[g] = a.pool == 1 ? a.ohat[ii] : 0;
+    c[g] = a.cls[ii];
+    const int64_t e = ii * a.stride + (lane_in ? j0 : 0);
+    b4[g] = *reinterpret_cast<const float4*>(a.backlog + e);
+    q4[g] = *reinterpret_cast<const int4*>(a.queue + e);
+    k4[g] = *reinterpret_cast<const int4*>(a.kv + e);
+  }
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const bool ok = live[g] && req_ok(a.pool, p[g], oh[g], c[g]);
+    const float sg = a.sigma[c[g] & (kMaxClasses - 1)];
+    const float work = a.pool == 1 ? a.w_s * (float)oh[g] * a.tau : a.w_s * (float)p[g] * a.tau;
+    const uint32_t need = a.pool == 1 ? (uint32_t)p[g] + (uint32_t)oh[g] : (uint32_t)p[g];  // < 2^31 when ok
+    const float bb[4] = {b4[g].x, b4[g].y, b4[g].z, b4[g].w};
+    const int32_t qq[4] = {q4[g].x, q4[g].y, q4[g].z, q4[g].w};
+    const int32_t kk[4] = {k4[g].x, k4[g].y, k4[g].z, k4[g].w};
+    uint32_t bkey = 0xffffffffu;
+    int32_t bj = j0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      // occupancy + need, exact in 32 bits: unsigned when the occupancy is
+      // >= 0 (the sum is < 2^32), signed otherwise (the sum is < 2^31)
+      const uint32_t sum = (uint32_t)kk[u] + need;
+      const float kvn = kk[u] >= 0 ? (float)sum : (float)(int32_t)sum;
+      const float press = kvn * a.inv_cap;
+      const float load = a.w_b * bb[u] * sg;
+      const float size = work * (1.0f + a.rho * press) * sg;
+      const float cost = load + size + a.w_q * (float)qq[u];
+      uint32_t k = cost_key(cost);
+      k = lane_in ? k : 0xffffffffu;
+      const bool b = k < bkey;
+      bkey = b ? k : bkey;
+      bj = b ? j0 + u : bj;
+    }
+    const uint32_t m = row_min(bkey);
+    const uint32_t idx = row_min(bkey == m ? (uint32_t)bj : 0xffffffffu);
+    const int64_t i = first + 4 * g + rq;
+    if (live[g] && ql == 0) {
+      a.out_idx[i] = ok ? (int32_t)idx : -1;
+      a.out_score[i] = __uint_as_float(ok ? m : 0x7fc00000u);
+    }
+  }
+}
+
 __global__ void __launch_bounds__(kBlock) goodput_kernel(GoodputArgs a) {
   const int lane = threadIdx.x & 63;
   const int64_t rep = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
@@ -230,6 +312,13 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t stream) {
     const int64_t blocks = (a.n_req + per_block - 1) / per_block;
     const size_t lds = sizeof(SnapEntry) * (size_t)a.n_inst;
     hipLaunchKernelGGL(score_shared_kernel, dim3((unsigned)blocks), dim3(kBlock), lds, stream, a);
+    return hipGetLastError();
+  }
+  const bool aligned = ((uintptr_t)a.backlog | (uintptr_t)a.queue | (uintptr_t)a.kv) % 16 == 0;
+  if (a.n_inst <= 64 && a.n_inst % 4 == 0 && a.stride % 4 == 0 && aligned) {
+    const int64_t per_block = (kBlock / 64) * 4 * kRowGroups;
+    const unsigned blocks = (unsigned)((a.n_req + per_block - 1) / per_block);
+    hipLaunchKernelGGL(score_rows16_kernel, dim3(blocks), dim3(kBlock), 0, stream, a);
     return hipGetLastError();
   }
   int S = 1;

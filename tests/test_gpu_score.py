@@ -56,10 +56,37 @@ def test_scorer_shared_ragged_widths(n_inst):
     _compare(prm, "prefill", d, n_inst, 0, d["kv_cap"])
 
 
-@pytest.mark.parametrize("n_inst,stride", [(1, 1), (3, 3), (8, 11), (64, 64), (65, 65), (300, 301), (1024, 1024)])
+@pytest.mark.parametrize("n_inst,stride", [(1, 1), (3, 3), (8, 11), (4, 4), (16, 20), (32, 32), (60, 64), (64, 64),
+                                           (64, 68), (65, 65), (300, 301), (1024, 1024)])
 def test_scorer_per_request_snapshots(n_inst, stride):
     n_req = 20_001 if n_inst <= 64 else 2_001
     d = W.scorer_inputs(n_req=n_req, n_inst=stride, seed=100 + n_inst, per_request=True)
+    prm = W.scorer_params()
+    _compare(prm, "decode", d, n_inst, stride, d["kv_cap"])
+    _compare(prm, "prefill", d, n_inst, stride, d["kv_cap"])
+
+
+def test_scorer_full_size_per_request_rows():
+    """The benchmark's per-request workload: 2^20 requests, a 64-instance row
+    each (16 lanes per request, 16-byte loads)."""
+    d = W.scorer_inputs(n_req=1 << 20, n_inst=64, seed=1, per_request=True)
+    prm = W.scorer_params()
+    ties = _compare(prm, "decode", d, 64, 64, d["kv_cap"])
+    print(f"scorer 1048576x64 per-request: near-tie divergences {ties}", flush=True)
+
+
+@pytest.mark.parametrize("n_inst,stride", [(64, 64), (40, 44)])
+def test_scorer_rows_rejected_requests_and_negative_occupancy(n_inst, stride):
+    d = W.scorer_inputs(n_req=3001, n_inst=stride, seed=6, per_request=True)
+    d["prompt_len"][::7] = 0
+    d["pred_out_len"][3::11] = 0
+    d["slo_class"][5::13] = 9
+    d["prompt_len"][6] = 2 ** 30
+    d["pred_out_len"][6] = 2 ** 30
+    kv = d["kv_occ"].reshape(-1, stride)
+    kv[4, :] = -5000
+    kv[9, 3] = -2 ** 31 + 7
+    kv[10, :] = 2 ** 31 - 2  # with the need, beyond int32: the unsigned path
     prm = W.scorer_params()
     _compare(prm, "decode", d, n_inst, stride, d["kv_cap"])
     _compare(prm, "prefill", d, n_inst, stride, d["kv_cap"])
