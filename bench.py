@@ -259,7 +259,7 @@ def bench_scorer(args, rows=False):
     if rows:
         roof = dict(bound="hbm", achieved=alg_bytes / kernel_s / 1e9, peak=HBM_PEAK / 1e9, unit="GB/s")
         roof["traffic"] = _traffic("score", "scorer_rows", SCORE_SOURCES)
-        roof["kernel"] = "rt::score_rows_kernel"
+        roof["kernel"] = "rt::score_rows16_kernel"
         roof["per_unit"] = (f"{SCORE_BYTES_PER_PAIR_ROWS} B/pair + {SCORE_BYTES_PER_REQ} B/request")
     else:
         roof = dict(bound="alu", achieved=alg_ops / kernel_s / 1e12, peak=ALU_PEAK / 1e12, unit="Tlane-op/s")

@@ -182,6 +182,22 @@ def test_wide_bench_workload_sampled():
     log(f"batched 65536x2000: {rep}; mean goodput {g.mean():.4f}")
 
 
+def test_wide_pool_bench_workload_sampled():
+    """The batched bench workload whose pool (8 prefill + 64 decode) is too
+    wide for a segment, in the launch bench.py times (the one-replica-per-lane
+    kernel): properties on every request, goodput recount on every replica,
+    follow-mode parity on a spread sample of replicas."""
+    wl = W.batched_wide_pool()
+    tr = W.make_trace(wl)
+    gpu, g, met, flags = run_sim(wl.points, tr)
+    assert flags == 0
+    check_properties(wl.points, tr, gpu)
+    assert np.array_equal(goodput_recount(wl.points, tr, gpu), met)
+    sample = list(range(0, wl.n_replicas, 1023)) + [wl.n_replicas - 1]
+    rep = follow_replicas(wl.points, tr, gpu, sample, gpu_goodput=g, gpu_met=met)
+    log(f"batched wide pool {wl.n_replicas}x{wl.requests}: {rep}; mean goodput {g.mean():.4f}")
+
+
 def test_coarse_grid_ties_many_small_replicas():
     """Hundreds of small replicas on a coarse time grid with tiny integer
     physics and transfers of zero: simultaneous arrivals, equal finish times
