@@ -34,14 +34,18 @@
 // largest valid one before it, whether accepted or not).  The raw trace of a
 // block is loaded two blocks ahead.
 //
-// Argmin.  Each wave reduces both pools over its 64 lanes (DPP within rows,
-// row broadcasts across them; within a wave the lowest lane and slot hold
-// the lowest index), then lane 0 of every wave folds its two winners into an
-// LDS minimum of the packed key (cost key << 32 | instance index), so equal
-// costs keep the lowest index, and writes their busy-until next to it.
-// After one barrier per step (it orders LDS only: every global access of a
-// wave is to addresses no other wave touches) every wave reads both minima
-// and then the two winners' busy-until, so all waves form the same prefill
+// Argmin.  Every lane that holds instances folds its best slot (the lowest
+// slot of the lane's smallest cost key) into the LDS minimum of its pool,
+// packed as (cost key << 32 | instance index << 9 | cell), and writes that
+// slot's busy-until to its own cell (wave * 64 + lane).  The 64-bit minimum
+// keeps the smallest key and, among equal keys, the lowest index; the cell
+// bits never decide (indices are unique).  No reduction within the wave
+// precedes the fold: a DPP argmin with its scalar winner lookup was a chain
+// of vector-to-scalar round trips, and the LDS takes a few hundred atomics
+// per step without becoming the bound.  After one barrier per step (it
+// orders LDS only: every global access of a wave is to addresses no other
+// wave touches) every wave reads both minima and then the two winners'
+// busy-until from the cells they name, so all waves form the same prefill
 // and decode ends.
 // The LDS cells rotate over three step slots: slot t % 3 is filled at step
 // t, read after its barrier, and reset by wave 0 after the barrier of step
@@ -173,27 +177,10 @@ __device__ __forceinline__ double wave_prefix_max(double x) {
   return x;
 }
 
-// Minimum over the wave of two values at once; lane 63 holds the results.
-__device__ __forceinline__ void wave_min2_to_63(uint32_t& v, uint32_t& w) {
-  v = min(v, dpp<0xB1>(v));
-  w = min(w, dpp<0xB1>(w));
-  v = min(v, dpp<0x4E>(v));
-  w = min(w, dpp<0x4E>(w));
-  v = min(v, dpp<0x141>(v));
-  w = min(w, dpp<0x141>(w));
-  v = min(v, dpp<0x140>(v));
-  w = min(w, dpp<0x140>(w));
-  // rows 1 and 3 take the last lane of the row before them, then rows 2 and
-  // 3 take lane 31 (the other rows keep their value)
-  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x142, 0xA, 0xF, false));
-  w = min(w, (uint32_t)__builtin_amdgcn_update_dpp((int)w, (int)w, 0x142, 0xA, 0xF, false));
-  v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x143, 0xC, 0xF, false));
-  w = min(w, (uint32_t)__builtin_amdgcn_update_dpp((int)w, (int)w, 0x143, 0xC, 0xF, false));
-}
-
 template <int W, int M, int kMode>
 __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   static_assert(W == 2 || W == 4 || W == 8, "workgroups of 2, 4 or 8 waves");
+  static_assert(W * 64 <= 512, "a busy-until cell index fits 9 bits of the packed minimum");
   constexpr int kLogW = W == 2 ? 1 : (W == 4 ? 2 : 3);
   constexpr bool kTok = mode_ledger(kMode);    // the ledger is priced
   constexpr bool kKv = kMode != kModeBase;     // occupancy is priced
@@ -227,7 +214,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   const int64_t dmy = -1 - (int64_t)wave_id - base;
 
   __shared__ unsigned long long best[3][2];  // per step slot: packed minimum of each pool
-  __shared__ double wbusy[3][W][2];          // per step slot: each wave's winners' busy-until
+  __shared__ double wbusy[3][W * 64];         // per step slot: each lane's best busy-until
   __shared__ WReq reqs[2][64];               // request records of the current and the next block
   if (threadIdx.x < 6) best[threadIdx.x >> 1][threadIdx.x & 1] = ~0ull;
 
@@ -235,18 +222,19 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   bool ok[M];    // the slot holds an instance of the lane's pool
   float wqq[M];  // w_q * (float)queue of each slot
   float blv[M];  // ledger backlog of each slot (ledger modes)
-#pragma unroll
-  for (int m = 0; m < M; ++m) {
+  // (slot indices compile-time from the start: a loop here left the slot
+  // array in scratch memory in the ledger modes)
+  static_for<M>([&](auto mc) __attribute__((always_inline)) {
+    constexpr int m = decltype(mc)::value;
     init_wslot(s[m]);
     ok[m] = inpool && wave + W * (lrel * M + m) < npool;
-  }
+  });
   // a slot's cached queue and ledger terms, after its queue or ledger changed
   auto refresh = [&](int m) __attribute__((always_inline)) {
     wqq[m] = w_q * (float)s[m].q;
     if constexpr (kTok) blv[m] = tau * (float)s[m].pend + basec * (float)s[m].q;
   };
-#pragma unroll
-  for (int m = 0; m < M; ++m) refresh(m);
+  static_for<M>([&](auto mc) __attribute__((always_inline)) { refresh(decltype(mc)::value); });
 
   // Raw trace of a block, lane k holding request (block start + k) (clamped
   // into the replica; lanes past its end are rejected when the block's
@@ -390,34 +378,20 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
       }
     }
 
-    // 2. per-wave argmin of both pools; lane 0 folds the wave's winners into
-    // the LDS minima and publishes their busy-until
-    {
-      uint32_t kp = isp ? bkey : 0xffffffffu, kd = isp ? 0xffffffffu : bkey;
-      const uint32_t kp0 = kp, kd0 = kd;
-      wave_min2_to_63(kp, kd);
-      const uint32_t mkp = (uint32_t)__builtin_amdgcn_readlane((int)kp, 63);
-      const uint32_t mkd = (uint32_t)__builtin_amdgcn_readlane((int)kd, 63);
-      // the wave's winning lanes: the lowest lane holding each minimum
-      const int32_t wp = (__ffsll((unsigned long long)__ballot(kp0 == mkp)) - 1) & 63;
-      const int32_t wd = (__ffsll((unsigned long long)__ballot(kd0 == mkd)) - 1) & 63;
-      const int32_t mpw = __builtin_amdgcn_readlane(bm, wp);
-      const int32_t mdw = __builtin_amdgcn_readlane(bm, wd);
-      const double bpw = rl_f64(bbusy, wp), bdw = rl_f64(bbusy, wd);
-      const uint32_t ipw = (uint32_t)(wave + W * (wp * M + mpw));
-      const uint32_t idw = (uint32_t)(wave + W * ((wd - LPW) * M + mdw));
-      if (lane == 0) {
-        atomicMin(&best[sl3][0], ((unsigned long long)mkp << 32) | ipw);
-        atomicMin(&best[sl3][1], ((unsigned long long)mkd << 32) | idw);
-        wbusy[sl3][wave][0] = bpw;
-        wbusy[sl3][wave][1] = bdw;
-      }
+    // 2. every lane holding instances folds its best slot into its pool's
+    // LDS minimum and leaves that slot's busy-until in its cell
+    if (inpool) {
+      const uint32_t cell = (uint32_t)(wave * 64 + lane);
+      const uint32_t idx = (uint32_t)(wave + W * (lrel * M + bm));
+      atomicMin(&best[sl3][isp ? 0 : 1], ((unsigned long long)bkey << 32) | (idx << 9) | cell);
+      wbusy[sl3][cell] = bbusy;
     }
     lds_barrier();
-    const int32_t ip = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)best[sl3][0]);
-    const int32_t id = __builtin_amdgcn_readfirstlane((int32_t)(uint32_t)best[sl3][1]);
-    const double busy_ip = wbusy[sl3][ip & (W - 1)][0];
-    const double busy_id = wbusy[sl3][id & (W - 1)][1];
+    const uint32_t bpl = (uint32_t)best[sl3][0], bdl = (uint32_t)best[sl3][1];
+    const int32_t ip = __builtin_amdgcn_readfirstlane((int32_t)(bpl >> 9));
+    const int32_t id = __builtin_amdgcn_readfirstlane((int32_t)(bdl >> 9));
+    const double busy_ip = wbusy[sl3][__builtin_amdgcn_readfirstlane((int32_t)(bpl & 511u))];
+    const double busy_id = wbusy[sl3][__builtin_amdgcn_readfirstlane((int32_t)(bdl & 511u))];
     // the cells of step t - 1 are free again (every wave has read them)
     const int sl_prev = sl3 == 0 ? 2 : sl3 - 1;
     if (wave == 0 && lane < 2) best[sl_prev][lane] = ~0ull;
