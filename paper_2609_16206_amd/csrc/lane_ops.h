@@ -29,6 +29,15 @@ __device__ __forceinline__ int64_t f64_to_i64(double x) {
   return (int64_t)(((uint64_t)hi << 32) | (uint32_t)__double2loint(y));
 }
 
+// Maximum of two doubles that are never NaN, as one instruction (fmax first
+// canonicalizes each operand it cannot prove canonical: one more
+// instruction per operand).
+__device__ __forceinline__ double max_f64(double a, double b) {
+  double r;
+  asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // Hides a value's provenance from the optimizer (it stays in a VGPR), so that
 // a select on it is not re-associated into a combination of lane masks.
 template <typename T>

@@ -36,13 +36,15 @@
 //
 // Argmin.  Every lane that holds instances folds its best slot (the lowest
 // slot of the lane's smallest cost key) into the LDS minimum of its pool,
-// packed as (cost key << 32 | instance index << 9 | cell), and writes that
-// slot's busy-until to its own cell (wave * 64 + lane).  The 64-bit minimum
-// keeps the smallest key and, among equal keys, the lowest index; the cell
-// bits never decide (indices are unique).  No reduction within the wave
-// precedes the fold: a DPP argmin with its scalar winner lookup was a chain
-// of vector-to-scalar round trips, and the LDS takes a few hundred atomics
-// per step without becoming the bound.  After one barrier per step (it
+// packed as (cost key << 32 | instance index << 14 | FIFO position << 12 |
+// slot << 9 | cell), and writes that slot's busy-until to its own cell
+// (wave * 64 + lane).  The 64-bit minimum keeps the smallest key and, among
+// equal keys, the lowest index; the bits below the index never decide
+// (indices are unique), and they hand the winner's wave, lane, slot and
+// queue length (capped at 3: beyond the window) to the append as scalars.
+// No reduction within the wave precedes the fold: a DPP argmin with its
+// scalar winner lookup was a chain of vector-to-scalar round trips, and the
+// LDS takes a few hundred atomics per step without becoming the bound.  After one barrier per step (it
 // orders LDS only: every global access of a wave is to addresses no other
 // wave touches) every wave reads both minima and then the two winners'
 // busy-until from the cells they name, so all waves form the same prefill
@@ -180,8 +182,9 @@ __device__ __forceinline__ double wave_prefix_max(double x) {
 template <int W, int M, int kMode>
 __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
   static_assert(W == 2 || W == 4 || W == 8, "workgroups of 2, 4 or 8 waves");
-  static_assert(W * 64 <= 512, "a busy-until cell index fits 9 bits of the packed minimum");
-  constexpr int kLogW = W == 2 ? 1 : (W == 4 ? 2 : 3);
+  // (instance indices, below the boundary's pool limit of 1,024, fit the
+  // 18 bits above them)
+  static_assert(W * 64 <= 512 && M <= 8, "cell and slot fit their bits of the packed minimum");
   constexpr bool kTok = mode_ledger(kMode);    // the ledger is priced
   constexpr bool kKv = kMode != kModeBase;     // occupancy is priced
   constexpr bool kSamp = mode_sampled(kMode);  // two candidates per pool
@@ -338,6 +341,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     const bool long_req = rq.oh >= len_thr;  // length threshold: the upper part
     uint32_t bkey = 0xffffffffu;
     int32_t bm = 0;
+    int32_t bq = s[0].q;
     double bbusy = s[0].busy;
     const uint32_t c1 = isp ? rq.cand[0] : rq.cand[2], c2 = isp ? rq.cand[1] : rq.cand[3];
 #pragma unroll
@@ -374,6 +378,7 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
         const bool b = key < bkey;
         bkey = b ? key : bkey;
         bm = b ? m : bm;
+        bq = b ? x.q : bq;
         bbusy = b ? x.busy : bbusy;
       }
     }
@@ -383,15 +388,18 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
     if (inpool) {
       const uint32_t cell = (uint32_t)(wave * 64 + lane);
       const uint32_t idx = (uint32_t)(wave + W * (lrel * M + bm));
-      atomicMin(&best[sl3][isp ? 0 : 1], ((unsigned long long)bkey << 32) | (idx << 9) | cell);
+      const uint32_t wq = (uint32_t)min(bq, 3);  // the FIFO position the request would take
+      atomicMin(&best[sl3][isp ? 0 : 1],
+                ((unsigned long long)bkey << 32) | (idx << 14) | (wq << 12) | ((uint32_t)bm << 9) | cell);
       wbusy[sl3][cell] = bbusy;
     }
     lds_barrier();
     const uint32_t bpl = (uint32_t)best[sl3][0], bdl = (uint32_t)best[sl3][1];
-    const int32_t ip = __builtin_amdgcn_readfirstlane((int32_t)(bpl >> 9));
-    const int32_t id = __builtin_amdgcn_readfirstlane((int32_t)(bdl >> 9));
-    const double busy_ip = wbusy[sl3][__builtin_amdgcn_readfirstlane((int32_t)(bpl & 511u))];
-    const double busy_id = wbusy[sl3][__builtin_amdgcn_readfirstlane((int32_t)(bdl & 511u))];
+    const uint32_t bps = (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)bpl);
+    const uint32_t bds = (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)bdl);
+    const int32_t ip = (int32_t)(bps >> 14), id = (int32_t)(bds >> 14);
+    const double busy_ip = wbusy[sl3][bps & 511u];
+    const double busy_id = wbusy[sl3][bds & 511u];
     // the cells of step t - 1 are free again (every wave has read them)
     const int sl_prev = sl3 == 0 ? 2 : sl3 - 1;
     if (wave == 0 && lane < 2) best[sl_prev][lane] = ~0ull;
@@ -400,25 +408,24 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
 
     // 3. serve (uniform): prefill, KV transfer, decode (exact integers in
     // doubles)
-    const double pf_end = __builtin_fmax(now, busy_ip) + rq.s_pre;
+    const double pf_end = max_f64(now, busy_ip) + rq.s_pre;
     const double kv_at = pf_end + rq.xfer;
-    const double de = __builtin_fmax(kv_at, busy_id) + rq.s_dec;
+    const double de = max_f64(kv_at, busy_id) + rq.s_dec;
 
     // 5. append the request to the winning slot of each pool (uniform
     // branches: the winner's wave and slot, then its FIFO position)
     if (go) {
-      auto append = [&](int32_t win, int32_t lane_off, double end, int32_t fp, int32_t tk)
+      auto append = [&](uint32_t pk, double end, int32_t fp, int32_t tk)
                         __attribute__((always_inline)) {
-        const int32_t q = win >> kLogW;       // position within the wave
-        const int32_t lw = lane_off + q / M;  // lane
-        const int32_t mw = q - (q / M) * M;   // slot
+        const int32_t lw = (int32_t)(pk & 63u);        // lane
+        const int32_t mw = (int32_t)((pk >> 9) & 7u);  // slot
+        const int32_t w = (int32_t)((pk >> 12) & 3u);  // z's FIFO position (3: beyond the window)
         const bool own = lane == lw;
         const Elem z{end, t, fp, tk};
         static_for<M>([&](auto mc) __attribute__((always_inline)) {
           constexpr int m = decltype(mc)::value;
           if (m != mw) return;
           WSlot& x = s[m];
-          const int32_t w = __builtin_amdgcn_readlane(x.q, lw);  // z's FIFO position
           x.h = sel(own && w == 0, z, x.h);
           x.n = sel(own && w == 1, z, x.n);
           x.n2 = sel(own && w == 2, z, x.n2);
@@ -446,8 +453,8 @@ __global__ void __launch_bounds__(64 * W) wseg_kernel(SimArgs a) {
           refresh(m);
         });
       };
-      if (wave == (ip & (W - 1))) append(ip, 0, pf_end, rq.p, rq.p);
-      if (wave == (id & (W - 1))) append(id, LPW, de, rq.po, rq.oh);
+      if (wave == (ip & (W - 1))) append(bps, pf_end, rq.p, rq.p);
+      if (wave == (id & (W - 1))) append(bds, de, rq.po, rq.oh);
     }
 
     // 6. the outcome: each array kept by its wave, written per block of 64
