@@ -133,8 +133,10 @@ __device__ __forceinline__ void store_out_if(uint32_t c, int32_t* p0, int32_t v0
 // Segment collectives over aligned groups of S lanes.  Within a 16-lane row:
 // quad_perm xor 1, xor 2, then half-row mirror and row mirror (each step
 // pairs every lane with one from the other half of its group, so after
-// log2(S) steps every lane holds the group result).  Across rows: readlane
-// of each row.  For S > 64 these reduce over the wave.
+// log2(S) steps every lane holds the group result).  Across rows, on the
+// vector unit: v_permlane16_swap hands every lane of rows 0 and 1 (2 and 3)
+// the other row's value, v_permlane32_swap every lane the other half's.  For
+// S > 64 these reduce over the wave.
 // ---------------------------------------------------------------------------
 template <int C>
 __device__ __forceinline__ uint32_t dpp(uint32_t v) {
@@ -145,19 +147,28 @@ __device__ __forceinline__ uint32_t rl(uint32_t v, int lane) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
 
+// Combines each lane's value with its paired row's (S >= 32) and half's
+// (S >= 64), after the reduction within rows.
+template <int S, typename Op>
+__device__ __forceinline__ uint32_t cross_rows(uint32_t v, Op op) {
+  if constexpr (S >= 32) {
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    v = op(r[0], r[1]);
+  }
+  if constexpr (S >= 64) {
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    v = op(r[0], r[1]);
+  }
+  return v;
+}
+
 template <int S>
 __device__ __forceinline__ uint32_t seg_min(uint32_t v, int lane) {
   if constexpr (S >= 2) v = min(v, dpp<0xB1>(v));
   if constexpr (S >= 4) v = min(v, dpp<0x4E>(v));
   if constexpr (S >= 8) v = min(v, dpp<0x141>(v));
   if constexpr (S >= 16) v = min(v, dpp<0x140>(v));
-  if constexpr (S == 32) {
-    const uint32_t a = min(rl(v, 0), rl(v, 16)), b = min(rl(v, 32), rl(v, 48));
-    v = lane < 32 ? a : b;
-  } else if constexpr (S >= 64) {
-    v = min(min(rl(v, 0), rl(v, 16)), min(rl(v, 32), rl(v, 48)));
-  }
-  return v;
+  return cross_rows<S>(v, [](uint32_t x, uint32_t y) { return min(x, y); });
 }
 
 // Two independent segment minima, interleaved so that each DPP step of one
@@ -168,15 +179,8 @@ __device__ __forceinline__ void seg_min2(uint32_t& v, uint32_t& w, int lane) {
   if constexpr (S >= 4) { v = min(v, dpp<0x4E>(v)); w = min(w, dpp<0x4E>(w)); }
   if constexpr (S >= 8) { v = min(v, dpp<0x141>(v)); w = min(w, dpp<0x141>(w)); }
   if constexpr (S >= 16) { v = min(v, dpp<0x140>(v)); w = min(w, dpp<0x140>(w)); }
-  if constexpr (S == 32) {
-    const uint32_t a = min(rl(v, 0), rl(v, 16)), b = min(rl(v, 32), rl(v, 48));
-    const uint32_t c = min(rl(w, 0), rl(w, 16)), d = min(rl(w, 32), rl(w, 48));
-    v = lane < 32 ? a : b;
-    w = lane < 32 ? c : d;
-  } else if constexpr (S >= 64) {
-    v = min(min(rl(v, 0), rl(v, 16)), min(rl(v, 32), rl(v, 48)));
-    w = min(min(rl(w, 0), rl(w, 16)), min(rl(w, 32), rl(w, 48)));
-  }
+  v = cross_rows<S>(v, [](uint32_t x, uint32_t y) { return min(x, y); });
+  w = cross_rows<S>(w, [](uint32_t x, uint32_t y) { return min(x, y); });
 }
 
 template <int S>
@@ -185,13 +189,7 @@ __device__ __forceinline__ uint32_t seg_or(uint32_t v, int lane) {
   if constexpr (S >= 4) v |= dpp<0x4E>(v);
   if constexpr (S >= 8) v |= dpp<0x141>(v);
   if constexpr (S >= 16) v |= dpp<0x140>(v);
-  if constexpr (S == 32) {
-    const uint32_t a = rl(v, 0) | rl(v, 16), b = rl(v, 32) | rl(v, 48);
-    v = lane < 32 ? a : b;
-  } else if constexpr (S >= 64) {
-    v = (rl(v, 0) | rl(v, 16)) | (rl(v, 32) | rl(v, 48));
-  }
-  return v;
+  return cross_rows<S>(v, [](uint32_t x, uint32_t y) { return x | y; });
 }
 
 // Maximum over the whole wave of non-negative values.
@@ -216,15 +214,9 @@ __device__ __forceinline__ double seg_bcast_f64(double v, bool own, int lane) {
   if constexpr (S >= 4) { lo |= dpp<0x4E>(lo); hi |= dpp<0x4E>(hi); }
   if constexpr (S >= 8) { lo |= dpp<0x141>(lo); hi |= dpp<0x141>(hi); }
   if constexpr (S >= 16) { lo |= dpp<0x140>(lo); hi |= dpp<0x140>(hi); }
-  if constexpr (S == 32) {
-    const uint32_t a = rl(lo, 0) | rl(lo, 16), b = rl(lo, 32) | rl(lo, 48);
-    const uint32_t c = rl(hi, 0) | rl(hi, 16), d = rl(hi, 32) | rl(hi, 48);
-    lo = lane < 32 ? a : b;
-    hi = lane < 32 ? c : d;
-  } else if constexpr (S >= 64) {
-    lo = (rl(lo, 0) | rl(lo, 16)) | (rl(lo, 32) | rl(lo, 48));
-    hi = (rl(hi, 0) | rl(hi, 16)) | (rl(hi, 32) | rl(hi, 48));
-  }
+  const auto orf = [](uint32_t x, uint32_t y) { return x | y; };
+  lo = cross_rows<S>(lo, orf);
+  hi = cross_rows<S>(hi, orf);
   return __hiloint2double((int)hi, (int)lo);
 }
 
@@ -238,21 +230,11 @@ __device__ __forceinline__ void seg_bcast2_f64(double& x, bool ox, double& y, bo
   if constexpr (S >= 4) { a |= dpp<0x4E>(a); b |= dpp<0x4E>(b); c |= dpp<0x4E>(c); d |= dpp<0x4E>(d); }
   if constexpr (S >= 8) { a |= dpp<0x141>(a); b |= dpp<0x141>(b); c |= dpp<0x141>(c); d |= dpp<0x141>(d); }
   if constexpr (S >= 16) { a |= dpp<0x140>(a); b |= dpp<0x140>(b); c |= dpp<0x140>(c); d |= dpp<0x140>(d); }
-  if constexpr (S == 32) {
-    const uint32_t a0 = rl(a, 0) | rl(a, 16), a1 = rl(a, 32) | rl(a, 48);
-    const uint32_t b0 = rl(b, 0) | rl(b, 16), b1 = rl(b, 32) | rl(b, 48);
-    const uint32_t c0 = rl(c, 0) | rl(c, 16), c1 = rl(c, 32) | rl(c, 48);
-    const uint32_t d0 = rl(d, 0) | rl(d, 16), d1 = rl(d, 32) | rl(d, 48);
-    a = lane < 32 ? a0 : a1;
-    b = lane < 32 ? b0 : b1;
-    c = lane < 32 ? c0 : c1;
-    d = lane < 32 ? d0 : d1;
-  } else if constexpr (S >= 64) {
-    a = (rl(a, 0) | rl(a, 16)) | (rl(a, 32) | rl(a, 48));
-    b = (rl(b, 0) | rl(b, 16)) | (rl(b, 32) | rl(b, 48));
-    c = (rl(c, 0) | rl(c, 16)) | (rl(c, 32) | rl(c, 48));
-    d = (rl(d, 0) | rl(d, 16)) | (rl(d, 32) | rl(d, 48));
-  }
+  const auto orf = [](uint32_t x, uint32_t y) { return x | y; };
+  a = cross_rows<S>(a, orf);
+  b = cross_rows<S>(b, orf);
+  c = cross_rows<S>(c, orf);
+  d = cross_rows<S>(d, orf);
   x = __hiloint2double((int)b, (int)a);
   y = __hiloint2double((int)d, (int)c);
 }
