@@ -98,6 +98,20 @@ def _traffic(kernel_tag, workload_name, sources):
     return d.get("bytes_per_launch")
 
 
+def _valu_busy(kernel_tag, workload_name, sources):
+    """Measured VALU issue share of the dominant kernel(s) from the committed
+    counter summary (VALUBusy, percent, one entry per kernel class the call
+    launches), if it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"valu_{kernel_tag}_{workload_name}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("source_sha") != _source_hash(sources):
+        return None
+    return d.get("valu_busy_pct")
+
+
 def cpu_threads():
     """Threads for the oracle's baseline: the cores this process may run on,
     capped by OMP_NUM_THREADS where the host sets the job's CPU share."""
@@ -194,6 +208,8 @@ def bench_sim(args):
     batched = any(p.get("service") == "batched" for p in wl.points)
     roof["traffic"] = _traffic("bat", args.workload, BAT_SOURCES) if batched else _traffic("sim", args.workload,
                                                                                           SIM_SOURCES)
+    roof["valu_busy_pct"] = (_valu_busy("bat", args.workload, BAT_SOURCES) if batched else
+                             _valu_busy("sim", args.workload, SIM_SOURCES))
     roof["kernel"] = ("rt::bat::bseg_kernel / bat_kernel (the batched classes the call launches)" if batched else
                       "rt::seg::seg_kernel / wseg_kernel (every class one rt_sim_run_replicas call launches)")
     roof["per_unit"] = (f"{SIM_BYTES_PER_REQ} B/request; {SIM_OPS_PER_PAIR} lane-ops/pair + {SIM_OPS_PER_REQ}/request "
@@ -259,11 +275,13 @@ def bench_scorer(args, rows=False):
     if rows:
         roof = dict(bound="hbm", achieved=alg_bytes / kernel_s / 1e9, peak=HBM_PEAK / 1e9, unit="GB/s")
         roof["traffic"] = _traffic("score", "scorer_rows", SCORE_SOURCES)
+        roof["valu_busy_pct"] = _valu_busy("score", "scorer_rows", SCORE_SOURCES)
         roof["kernel"] = "rt::score_rows16_kernel"
         roof["per_unit"] = (f"{SCORE_BYTES_PER_PAIR_ROWS} B/pair + {SCORE_BYTES_PER_REQ} B/request")
     else:
         roof = dict(bound="alu", achieved=alg_ops / kernel_s / 1e12, peak=ALU_PEAK / 1e12, unit="Tlane-op/s")
         roof["traffic"] = _traffic("score", "scorer", SCORE_SOURCES)
+        roof["valu_busy_pct"] = _valu_busy("score", "scorer", SCORE_SOURCES)
         roof["kernel"] = "rt::score_shared_kernel"
         roof["per_unit"] = (f"{SCORE_OPS_PER_PAIR} lane-ops/pair (recount {RECOUNT_SCORE[0]}/pair + "
                             f"{RECOUNT_SCORE[1]}/request)")
