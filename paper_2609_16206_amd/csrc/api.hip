@@ -311,7 +311,16 @@ void plan_launch(const rt_sim_points& sp, int64_t n, PlanBufs& b) {
   for (int c = 0; c < ncls; ++c)
     if (b.count[c] > 0) b.act[b.n_act++] = c;
   const double* cost = b.cost;
-  std::sort(b.act, b.act + b.n_act, [cost](int x, int y) { return cost[x] != cost[y] ? cost[x] > cost[y] : x < y; });
+  // Launch order: the longest chain of one wave first (the class's step
+  // cost; every replica of a call has a comparable length), then the most
+  // work.  A class of few waves with dear steps started behind a large one
+  // finishes last (measured on the 1,225-point sweep: 66.0 ms dearest total
+  // first, 63.0 ms cheapest total first, 61.1 ms longest step first).
+  std::sort(b.act, b.act + b.n_act, [cost](int x, int y) {
+    const double cx = seg_step_cost(rt::sim_class(x)), cy = seg_step_cost(rt::sim_class(y));
+    if (cx != cy) return cx > cy;
+    return cost[x] != cost[y] ? cost[x] > cost[y] : x < y;
+  });
 }
 
 }  // namespace
