@@ -249,9 +249,10 @@ typedef struct {
  * with the proxy backlog, 192 when a call holds both kinds), and for
  * batched replicas with about 68 + 32 batch_cap bytes per instance slot: a
  * replica of a point with P + D <= 64 takes S slots, S the smallest of 4, 8,
- * 16, 32, 64 that holds P + D; a larger point takes P + D slots (each kind
- * sized by the largest pool and batch_cap among the call's points of that
- * kind).  It is owned by `sim`. */
+ * 16, 32, 64 that holds P + D; one with ceil(P / 2) + ceil(D / 2) <= 64
+ * (at most 128 instances) takes 128; a larger point takes P + D slots (each
+ * kind sized by the largest pool and batch_cap among the call's points of
+ * that kind).  It is owned by `sim`. */
 rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* out, void* hip_stream);
 
 /* For callers that cannot allocate memory (code under HIP graph capture,

@@ -144,7 +144,8 @@ int point_mode(const rt_point& p) {
 bool class_fits(const rt::SimClass& c, const rt_point& p) {
   // the batched service model has one class of its own
   if ((c.kind == rt::kBat) != (p.service == RT_SERVICE_BATCHED)) return false;
-  if (c.kind == rt::kBat) return c.MP == 0 || p.n_prefill + p.n_decode <= c.S;
+  if (c.kind == rt::kBat)
+    return c.MP == 0 || (p.n_prefill + c.MP - 1) / c.MP + (p.n_decode + c.MP - 1) / c.MP <= c.S;
   if (c.kind == rt::kSeg) {
     if (c.mode != point_mode(p)) return false;
     const int lanes = (p.n_prefill + c.MP - 1) / c.MP + (p.n_decode + c.MD - 1) / c.MD;
@@ -626,7 +627,7 @@ rt_status rt_sim_run_replicas(rt_sim* sim, const rt_trace* trace, rt_sim_out* ou
         NI = std::max(NI, q.n_prefill + q.n_decode);
         C = std::max(C, q.batch_cap == 0 ? kDefaultBatchCap : q.batch_cap);
       }
-      if (sc.MP == 1) NI = 1;  // a segment class: one instance per lane
+      if (sc.MP >= 1) NI = sc.MP;  // a segment class: MP instances per lane
       dims.push_back(Dim{c, rt::bat_lanes(sc, b.count[c]), NI, C});
       bneed += rt::bat_scratch_bytes(dims.back().S, NI, C);
     }

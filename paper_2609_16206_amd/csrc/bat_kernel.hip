@@ -23,10 +23,11 @@
 // taken prefill pool first, then decode pool, each instance in time order:
 // every instance sees the same sequence of events, in the same order and
 // with the same arithmetic, as a global time-ordered loop.  Two kernels do
-// this: bseg_kernel (below), one replica per segment of S <= 64 lanes and one
-// instance per lane, for points with P + D <= 64; and bat_kernel, one replica
-// per lane walking its instances in turn, for any point.  Batch members and
-// KV transfers in flight are sorted rings in scratch, contiguous per lane.
+// this: bseg_kernel (below), one replica per segment of S <= 64 lanes and M
+// instances per lane in registers (M = 1 for points with P + D <= 64, M = 2
+// for pools of up to 128 instances); and bat_kernel, one replica per lane
+// walking its instances in turn, for any point.  Batch members and KV
+// transfers in flight are sorted rings in scratch, contiguous per instance.
 //
 // Arithmetic.  Times are float64 ns; every operation matches the written
 // model one for one (built with -ffp-contract=off): s = 1 + beta * (b - 1),
@@ -518,10 +519,45 @@ struct Req {
   uint4 ws;
 };
 
+// One instance of the segment kernel, in registers (a lane holds M): the
+// batch's state, the first two entries of its rings with the front
+// requests' data, and the rings' cached tails.
+struct BInst {
+  double v, tl, left, kv, pend, owed;
+  int32_t q, nact, head, nw, wh;
+  // the batch's window and its front request's data (prefill: arrival, p,
+  // o, o^, decode instance; decode: prefill end, p, o, o^)
+  Window bw;
+  double x0;
+  int32_t p0, o0, oh0, dst0;
+  // the transfers' window (decode) and the front transfer's data
+  Window tw;
+  double pf1;
+  int32_t p1, o1, oh1;
+  RingTail btail, wtail;
+};
+
+__device__ __forceinline__ void init_binst(BInst& x) {
+  x.v = x.tl = x.left = x.kv = x.pend = x.owed = 0.0;
+  x.q = x.nact = x.head = x.nw = x.wh = 0;
+  x.bw = Window{0.0, 0.0, 0, 0};
+  x.x0 = 0.0;
+  x.p0 = x.o0 = x.oh0 = x.dst0 = 0;
+  x.tw = Window{0.0, 0.0, 0, 0};
+  x.pf1 = 0.0;
+  x.p1 = x.o1 = x.oh1 = 0;
+  x.btail = RingTail{0.0, 0};
+  x.wtail = RingTail{0.0, 0};
+}
+
 // kMinBlocks: workgroups per compute unit the register budget must allow
 // (1: as many registers as the kernel wants, for launches whose waves do not
-// fill the GPU; 3: three waves per SIMD, for launches with many waves).
-template <int S, int kMinBlocks>
+// fill the GPU; 3 (M = 1) or 2 (M = 2): three or two waves per SIMD, for
+// launches with many waves).  M: instances per lane (prefill instance j on
+// lane j / M, slot j % M; decode instance d on lane ceil(P / M) + d / M,
+// slot d % M).  A round takes at most one event of every instance, slot
+// after slot; the state of every slot stays in registers (about 46 each).
+template <int S, int kMinBlocks, int M>
 __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, BatScratch b) {
   const int lane = (int)(threadIdx.x & 63);
   const int64_t gl = (int64_t)blockIdx.x * kBlock + threadIdx.x;
@@ -534,9 +570,13 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
   const int64_t len = has ? a.offsets[rep + 1] - lo : 0;
   const DevPoint& pt = a.points[(has && a.param_point) ? a.param_point[rep] : 0];
   const int32_t P = pt.P, D = pt.D;
-  const bool isP = has && sl < P;
-  const bool isD = has && sl >= P && sl < P + D;
-  const int32_t dme = sl - P;
+  const int32_t LP = (P + M - 1) / M, LD = (D + M - 1) / M;  // lanes holding each pool
+  const bool isP = has && sl < LP;
+  const bool isD = has && sl >= LP && sl < LP + LD;
+  const int32_t j0 = (isP ? sl : sl - LP) * M;  // the lane's first instance in its pool
+  bool ok[M];                                    // slot m holds an instance
+#pragma unroll
+  for (int m = 0; m < M; ++m) ok[m] = (isP && j0 + m < P) || (isD && j0 + m < D);
   const double beta = isP ? pt.beta_pre : pt.beta_dec;
   const double xfer = (double)pt.xfer_tok_ns;
   const bool samp = pt.policy == kPolicyLearnedSampled;
@@ -555,118 +595,139 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
   for (int k = sl; k < kMaxClasses; k += S) sig[sblk * kMaxClasses + k] = pt.sigma[k];
   __syncthreads();
   const int32_t C = b.C;
-  Entry* const ring = reinterpret_cast<Entry*>(b.ring) + gl * (int64_t)C;
-  Entry* const wring = reinterpret_cast<Entry*>(b.wring) + gl * (int64_t)C;
+  // the rings of slot m: batch members and KV transfers in flight
+  Entry* rings[M];
+  Entry* wrings[M];
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    rings[m] = reinterpret_cast<Entry*>(b.ring) + (gl * M + m) * (int64_t)C;
+    wrings[m] = reinterpret_cast<Entry*>(b.wring) + (gl * M + m) * (int64_t)C;
+  }
 
-  // instance state
-  double v = 0.0, tl = 0.0, left = 0.0, kv = 0.0, pend = 0.0, owed = 0.0;
-  int32_t q = 0, nact = 0, head = 0, nw = 0, wh = 0;
-  // the batch's window and its front request's data (prefill: arrival, p,
-  // o, o^, decode instance; decode: prefill end, p, o, o^)
-  Window bw{0.0, 0.0, 0, 0};
-  double x0 = 0.0;
-  int32_t p0 = 0, o0 = 0, oh0 = 0, dst0 = 0;
-  // the transfers' window (decode) and the front transfer's data
-  Window tw{0.0, 0.0, 0, 0};
-  double pf1 = 0.0;
-  int32_t p1 = 0, o1 = 0, oh1 = 0;
-  RingTail btail{0.0, 0}, wtail{0.0, 0};
+  BInst in[M];
+#pragma unroll
+  for (int m = 0; m < M; ++m) init_binst(in[m]);
   double tmax = 0.0;
   bool rej = false, full = false, dead = false;
   int64_t last = -1;
 
-  // The data of the batch's new front (needed only when it leaves).
-  auto front_data = [&]() {
-    const int64_t g = lo + bw.r0;
-    p0 = a.plen[g];
-    o0 = a.olen[g];
-    oh0 = a.ohat[g];
+  // The data of a batch's new front (needed only when it leaves).
+  auto front_data = [&](BInst& x) __attribute__((always_inline)) {
+    const int64_t g = lo + x.bw.r0;
+    x.p0 = a.plen[g];
+    x.o0 = a.olen[g];
+    x.oh0 = a.ohat[g];
     if (isP) {
-      x0 = i64_to_f64(a.arrival[g]);
-      dst0 = a.i_dec[g];
+      x.x0 = i64_to_f64(a.arrival[g]);
+      x.dst0 = a.i_dec[g];
     } else {
-      x0 = __longlong_as_double(a.span[g]);
+      x.x0 = __longlong_as_double(a.span[g]);
     }
   };
-  auto transfer_data = [&]() {
-    const int64_t g = lo + tw.r0;
-    p1 = a.plen[g];
-    o1 = a.olen[g];
-    oh1 = a.ohat[g];
-    pf1 = __longlong_as_double(a.span[g]);
+  auto transfer_data = [&](BInst& x) __attribute__((always_inline)) {
+    const int64_t g = lo + x.tw.r0;
+    x.p1 = a.plen[g];
+    x.o1 = a.olen[g];
+    x.oh1 = a.ohat[g];
+    x.pf1 = __longlong_as_double(a.span[g]);
   };
 
   // Every event at or before `now` (prefill rounds, then decode rounds).
   auto run_to = [&](double now) {
     // one prefill round; false when no lane had an event
     auto pre_round = [&]() -> bool {
-      double tc = kInf;
-      if (nact > 0) {
-        double rem = bw.k0 - v;
-        rem = rem < 0.0 ? 0.0 : rem;
-        tc = tl + rem * slowdown(beta, nact);
-      }
-      const bool fire = isP && !dead && nact > 0 && tc <= now;
-      const uint64_t fm = __ballot(fire);
-      if (fm == 0) return false;
-      double land = 0.0;
-      int32_t fr = 0, fd = 0, fp = 0, fo = 0, foh = 0;
-      if (fire) {
-        left = left - (double)nact * (bw.k0 - v);
-        v = bw.k0;
-        tl = tc;
-        tmax = fmax(tmax, tc);
-        const int64_t g = lo + bw.r0;
-        q -= 1;
-        kv = kv - (double)p0;
-        pend = pend - (double)p0;
-        a.ttft[g] = round_ns(tc - x0);
-        a.span[g] = __double_as_longlong(tc);
-        land = tc + (double)p0 * xfer;
-        tmax = fmax(tmax, land);
-        fr = bw.r0;
-        fd = dst0;
-        fp = p0;
-        fo = o0;
-        foh = oh0;
-        head += 1;
-        nact -= 1;
-        if (nact == 0) {
-          left = 0.0;
-        } else {
-          window_pop(bw, ring, C, head, nact);
-          front_data();
+      bool fire[M];
+      uint64_t fm[M];
+      uint64_t any = 0;
+      double land[M], ftl[M], tcs[M];
+      int32_t fr[M], fd[M], fp[M], fo[M], foh[M];
+      static_for<M>([&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        const BInst& x = in[m];
+        double tc = kInf;
+        if (x.nact > 0) {
+          double rem = x.bw.k0 - x.v;
+          rem = rem < 0.0 ? 0.0 : rem;
+          tc = x.tl + rem * slowdown(beta, x.nact);
         }
-      }
-      // the departing transfers go to their decode lanes: every position
-      // (within the segments) that fired somewhere in the wave is read by
-      // every lane from its own segment
-      uint64_t rel = 0;
-#pragma unroll
-      for (int s0 = 0; s0 < 64; s0 += S) rel |= (S == 64) ? fm : ((fm >> s0) & ((1ull << (S & 63)) - 1ull));
-      while (rel) {
-        const int i = __ffsll((unsigned long long)rel) - 1;
-        rel &= rel - 1;
-        const int src = base + i;
-        const bool fi = __shfl((int)fire, src) != 0;
-        const int32_t di = __shfl(fd, src);
-        const double li = __shfl(land, src);
-        const double ti = __shfl(tl, src);
-        const int32_t ri = __shfl(fr, src), pi = __shfl(fp, src), oi = __shfl(fo, src), ohi = __shfl(foh, src);
-        if (isD && fi && di == dme) {
-          const int32_t at = ring_put(wring, C, wh, nw, li, ri, wtail, full);
-          if (at >= 0) {
-            window_put(tw, at, wh, li, ri);
-            if (at == wh) {
-              pf1 = ti;
-              p1 = pi;
-              o1 = oi;
-              oh1 = ohi;
-            }
-            nw += 1;
+        tcs[m] = tc;
+        fire[m] = isP && !dead && x.nact > 0 && tc <= now;
+        fm[m] = __ballot(fire[m]);
+        any |= fm[m];
+      });
+      if (any == 0) return false;
+      static_for<M>([&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        BInst& x = in[m];
+        const double tc = tcs[m];
+        land[m] = 0.0;
+        fr[m] = fd[m] = fp[m] = fo[m] = foh[m] = 0;
+        if (fire[m]) {
+          x.left = x.left - (double)x.nact * (x.bw.k0 - x.v);
+          x.v = x.bw.k0;
+          x.tl = tc;
+          tmax = fmax(tmax, tc);
+          const int64_t g = lo + x.bw.r0;
+          x.q -= 1;
+          x.kv = x.kv - (double)x.p0;
+          x.pend = x.pend - (double)x.p0;
+          a.ttft[g] = round_ns(tc - x.x0);
+          a.span[g] = __double_as_longlong(tc);
+          land[m] = tc + (double)x.p0 * xfer;
+          tmax = fmax(tmax, land[m]);
+          fr[m] = x.bw.r0;
+          fd[m] = x.dst0;
+          fp[m] = x.p0;
+          fo[m] = x.o0;
+          foh[m] = x.oh0;
+          x.head += 1;
+          x.nact -= 1;
+          if (x.nact == 0) {
+            x.left = 0.0;
+          } else {
+            window_pop(x.bw, rings[m], C, x.head, x.nact);
+            front_data(x);
           }
         }
-      }
+        ftl[m] = x.tl;
+      });
+      // the departing transfers go to their decode instances: every position
+      // (within the segments) that fired somewhere in the wave is read by
+      // every lane from its own segment, slot by slot
+      static_for<M>([&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        uint64_t rel = 0;
+#pragma unroll
+        for (int s0 = 0; s0 < 64; s0 += S) rel |= (S == 64) ? fm[m] : ((fm[m] >> s0) & ((1ull << (S & 63)) - 1ull));
+        while (rel) {
+          const int i = __ffsll((unsigned long long)rel) - 1;
+          rel &= rel - 1;
+          const int src = base + i;
+          const bool fi = __shfl((int)fire[m], src) != 0;
+          const int32_t di = __shfl(fd[m], src);
+          const double li = __shfl(land[m], src);
+          const double ti = __shfl(ftl[m], src);
+          const int32_t ri = __shfl(fr[m], src), pi = __shfl(fp[m], src), oi = __shfl(fo[m], src),
+                        ohi = __shfl(foh[m], src);
+          static_for<M>([&](auto nc) __attribute__((always_inline)) {
+            constexpr int mm = decltype(nc)::value;
+            BInst& y = in[mm];
+            if (isD && fi && di == j0 + mm) {
+              const int32_t at = ring_put(wrings[mm], C, y.wh, y.nw, li, ri, y.wtail, full);
+              if (at >= 0) {
+                window_put(y.tw, at, y.wh, li, ri);
+                if (at == y.wh) {
+                  y.pf1 = ti;
+                  y.p1 = pi;
+                  y.o1 = oi;
+                  y.oh1 = ohi;
+                }
+                y.nw += 1;
+              }
+            }
+          });
+        }
+      });
       return true;
     };
     // two rounds per loop trip (measured: 8 % faster on a 4,096-replica cluster,
@@ -675,67 +736,71 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
     }
     // one decode round; false when no lane had an event
     auto dec_round = [&]() -> bool {
-      double tc = kInf, tj = kInf;
-      if (nact > 0) {
-        double rem = bw.k0 - v;
-        rem = rem < 0.0 ? 0.0 : rem;
-        tc = tl + rem * slowdown(beta, nact);
-      }
-      if (nw > 0) tj = tw.k0;
-      const bool fire = isD && !dead && (nact > 0 || nw > 0) && (tc <= tj ? tc : tj) <= now;
-      if (!__any(fire)) return false;
-      if (fire) {
+      bool anyf = false;
+      static_for<M>([&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        BInst& x = in[m];
+        double tc = kInf, tj = kInf;
+        if (x.nact > 0) {
+          double rem = x.bw.k0 - x.v;
+          rem = rem < 0.0 ? 0.0 : rem;
+          tc = x.tl + rem * slowdown(beta, x.nact);
+        }
+        if (x.nw > 0) tj = x.tw.k0;
+        const bool fire = isD && !dead && (x.nact > 0 || x.nw > 0) && (tc <= tj ? tc : tj) <= now;
+        anyf = anyf || fire;
+        if (!fire) return;
         if (tc <= tj) {
-          left = left - (double)nact * (bw.k0 - v);
-          v = bw.k0;
-          tl = tc;
+          x.left = x.left - (double)x.nact * (x.bw.k0 - x.v);
+          x.v = x.bw.k0;
+          x.tl = tc;
           tmax = fmax(tmax, tc);
-          const int64_t g = lo + bw.r0;
-          q -= 1;
-          kv = kv - ((double)p0 + (double)o0);
-          pend = pend - (double)oh0;
-          a.span[g] = round_ns(tc - x0);
-          head += 1;
-          nact -= 1;
-          if (nact == 0) {
-            left = 0.0;
+          const int64_t g = lo + x.bw.r0;
+          x.q -= 1;
+          x.kv = x.kv - ((double)x.p0 + (double)x.o0);
+          x.pend = x.pend - (double)x.oh0;
+          a.span[g] = round_ns(tc - x.x0);
+          x.head += 1;
+          x.nact -= 1;
+          if (x.nact == 0) {
+            x.left = 0.0;
           } else {
-            window_pop(bw, ring, C, head, nact);
-            front_data();
+            window_pop(x.bw, rings[m], C, x.head, x.nact);
+            front_data(x);
           }
         } else {
-          const int32_t r = tw.r0, pr = p1, orr = o1, ohr = oh1;
-          const double pfr = pf1;
-          wh += 1;
-          nw -= 1;
-          if (nw > 0) {
-            window_pop(tw, wring, C, wh, nw);
-            transfer_data();
+          const int32_t r = x.tw.r0, pr = x.p1, orr = x.o1, ohr = x.oh1;
+          const double pfr = x.pf1;
+          x.wh += 1;
+          x.nw -= 1;
+          if (x.nw > 0) {
+            window_pop(x.tw, wrings[m], C, x.wh, x.nw);
+            transfer_data(x);
           }
-          if (nact > 0) {
-            const double dv = (tj - tl) / slowdown(beta, nact);
-            v = v + dv;
-            left = left - (double)nact * dv;
+          if (x.nact > 0) {
+            const double dv = (tj - x.tl) / slowdown(beta, x.nact);
+            x.v = x.v + dv;
+            x.left = x.left - (double)x.nact * dv;
           }
-          tl = tj;
+          x.tl = tj;
           const double w = (double)(orr - 1) * dec_tok_ns;
-          owed = owed - w;
-          const double f = v + w;
-          const int32_t at = ring_put(ring, C, head, nact, f, r, btail, full);
+          x.owed = x.owed - w;
+          const double f = x.v + w;
+          const int32_t at = ring_put(rings[m], C, x.head, x.nact, f, r, x.btail, full);
           if (at >= 0) {
-            window_put(bw, at, head, f, r);
-            if (at == head) {
-              x0 = pfr;
-              p0 = pr;
-              o0 = orr;
-              oh0 = ohr;
+            window_put(x.bw, at, x.head, f, r);
+            if (at == x.head) {
+              x.x0 = pfr;
+              x.p0 = pr;
+              x.o0 = orr;
+              x.oh0 = ohr;
             }
-            nact += 1;
-            left = left + w;
+            x.nact += 1;
+            x.left = x.left + w;
           }
         }
-      }
-      return true;
+      });
+      return __any(anyf);
     };
     while (dec_round()) {
     }
@@ -787,92 +852,126 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
     // inside them (where it has no bits for lanes it considers gone) after
     // them; passing the counts through opaque() makes every later test of
     // them a fresh compare.
-    nact = opaque(nact);
-    nw = opaque(nw);
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      in[m].nact = opaque(in[m].nact);
+      in[m].nw = opaque(in[m].nw);
+    }
     // every instance's clock to the arrival
     if (valid && (isP || isD)) {
-      if (nact > 0) {
-        const double dv = (now - tl) / slowdown(beta, nact);
-        v = v + dv;
-        left = left - (double)nact * dv;
-      }
-      tl = now;
+      static_for<M>([&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        BInst& x = in[m];
+        if (x.nact > 0) {
+          const double dv = (now - x.tl) / slowdown(beta, x.nact);
+          x.v = x.v + dv;
+          x.left = x.left - (double)x.nact * dv;
+        }
+        x.tl = now;
+      });
     }
-    // each lane's key for its instance (0xffffffff: not offered)
-    uint32_t key = 0xffffffffu;
+    // each lane's key: the lowest of its instances' (lowest slot on equal
+    // keys; 0xffffffff: not offered)
+    uint32_t bkey = 0xffffffffu;
+    int32_t bm = 0;
     if (valid && (isP || isD)) {
       const int32_t n = isP ? P : D;
-      const int32_t jj = isP ? sl : dme;
-      if (pol == kPolicyRoundRobin) {
-        key = jj == t % n ? 0u : 1u;
-      } else if (pol == kPolicyLeastLoaded) {
-        key = (uint32_t)q;
-      } else if (pol == kPolicyLengthThreshold) {
-        const bool part = isP || n == 1 || ((jj >= (n + 1) / 2) == (oh >= len_thr));
-        key = part ? (uint32_t)q : 0xffffffffu;
-      } else {
-        const float sg = sig[sblk * kMaxClasses + (int)(c & (kMaxClasses - 1))];
-        const float work = isP ? w_s * (float)p * tau_pre : w_s * (float)oh * tau_dec;
-        const double need = isP ? (double)p : (double)p + (double)oh;
-        float bl;
-        if (bmode == 0) {
-          double w = left < 0.0 ? 0.0 : left;
-          w = w + owed;
-          bl = (float)w * 1e-9f;
-        } else if (isP) {
-          bl = tau_pre * (float)pend + pre_base * (float)q;
-        } else {
-          bl = tau_dec * (float)pend;
-        }
-        const float press = (float)(kv + need) * inv;
-        const float load = w_b * bl * sg;
-        const float size = work * (1.0f + rho * press) * sg;
-        key = cost_key(load + size + w_q * (float)q);
-        if (pol == kPolicyLearnedSampled) {
-          const uint32_t u = isP ? ws.x : ws.z, w2 = isP ? ws.y : ws.w;
-          const uint32_t c1 = __umulhi(u, (uint32_t)n);
-          const uint32_t x = __umulhi(w2, (uint32_t)(n - 1));
-          const uint32_t c2 = n > 1 ? x + (x >= c1 ? 1u : 0u) : c1;
-          key = ((uint32_t)jj == c1 || (uint32_t)jj == c2) ? key : 0xffffffffu;
-        }
+      uint32_t c1 = 0, c2 = 0;
+      if (pol == kPolicyLearnedSampled) {
+        const uint32_t u = isP ? ws.x : ws.z, w2 = isP ? ws.y : ws.w;
+        c1 = __umulhi(u, (uint32_t)n);
+        const uint32_t x = __umulhi(w2, (uint32_t)(n - 1));
+        c2 = n > 1 ? x + (x >= c1 ? 1u : 0u) : c1;
       }
+      static_for<M>([&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        const BInst& x = in[m];
+        const int32_t jj = j0 + m;
+        uint32_t key;
+        if (pol == kPolicyRoundRobin) {
+          key = jj == t % n ? 0u : 1u;
+        } else if (pol == kPolicyLeastLoaded) {
+          key = (uint32_t)x.q;
+        } else if (pol == kPolicyLengthThreshold) {
+          const bool part = isP || n == 1 || ((jj >= (n + 1) / 2) == (oh >= len_thr));
+          key = part ? (uint32_t)x.q : 0xffffffffu;
+        } else {
+          const float sg = sig[sblk * kMaxClasses + (int)(c & (kMaxClasses - 1))];
+          const float work = isP ? w_s * (float)p * tau_pre : w_s * (float)oh * tau_dec;
+          const double need = isP ? (double)p : (double)p + (double)oh;
+          float bl;
+          if (bmode == 0) {
+            double w = x.left < 0.0 ? 0.0 : x.left;
+            w = w + x.owed;
+            bl = (float)w * 1e-9f;
+          } else if (isP) {
+            bl = tau_pre * (float)x.pend + pre_base * (float)x.q;
+          } else {
+            bl = tau_dec * (float)x.pend;
+          }
+          const float press = (float)(x.kv + need) * inv;
+          const float load = w_b * bl * sg;
+          const float size = work * (1.0f + rho * press) * sg;
+          key = cost_key(load + size + w_q * (float)x.q);
+          if (pol == kPolicyLearnedSampled) key = ((uint32_t)jj == c1 || (uint32_t)jj == c2) ? key : 0xffffffffu;
+        }
+        key = ok[m] ? key : 0xffffffffu;
+        if (m == 0) {
+          bkey = key;
+        } else {
+          const bool lower = key < bkey;
+          bkey = lower ? key : bkey;
+          bm = lower ? m : bm;
+        }
+      });
     }
-    uint32_t kp = isP ? key : 0xffffffffu, kd = isD ? key : 0xffffffffu;
+    uint32_t kp = isP ? bkey : 0xffffffffu, kd = isD ? bkey : 0xffffffffu;
     const uint32_t kp0 = kp, kd0 = kd;
     seg_min2<S>(kp, kd, lane);
-    const int32_t ip = seg_first<S>(isP && kp0 == kp, lane);
-    const int32_t id = seg_first<S>(isD && kd0 == kd, lane) - P;
+    const int32_t wp = seg_first<S>(isP && kp0 == kp, lane);  // winning lanes
+    const int32_t wd = seg_first<S>(isD && kd0 == kd, lane);
+    int32_t mp = 0, md = 0;  // winning slots
+    if constexpr (M > 1) {
+      mp = (int32_t)seg_or<S>(sl == wp ? (uint32_t)bm : 0u, lane);
+      md = (int32_t)seg_or<S>(sl == wd ? (uint32_t)bm : 0u, lane);
+    }
+    const int32_t ip = wp * M + mp;
+    const int32_t id = (wd - LP) * M + md;
     if (valid) {
       if (sl == 0) {
         a.i_pre[g] = ip;
         a.i_dec[g] = id;
       }
-      if (isP && sl == ip) {
-        const double w = pre_base_ns + (double)p * pre_tok_ns;
-        const double f = v + w;
-        const int32_t at = ring_put(ring, C, head, nact, f, t, btail, full);
-        if (at >= 0) {
-          window_put(bw, at, head, f, t);
-          if (at == head) {
-            x0 = now;
-            p0 = p;
-            o0 = o;
-            oh0 = oh;
-            dst0 = id;
+      static_for<M>([&](auto mc) __attribute__((always_inline)) {
+        constexpr int m = decltype(mc)::value;
+        BInst& x = in[m];
+        if (isP && sl == wp && m == mp) {
+          const double w = pre_base_ns + (double)p * pre_tok_ns;
+          const double f = x.v + w;
+          const int32_t at = ring_put(rings[m], C, x.head, x.nact, f, t, x.btail, full);
+          if (at >= 0) {
+            window_put(x.bw, at, x.head, f, t);
+            if (at == x.head) {
+              x.x0 = now;
+              x.p0 = p;
+              x.o0 = o;
+              x.oh0 = oh;
+              x.dst0 = id;
+            }
+            x.nact += 1;
+            x.q += 1;
+            x.kv = x.kv + (double)p;
+            x.pend = x.pend + (double)p;
+            x.left = x.left + w;
           }
-          nact += 1;
-          q += 1;
-          kv = kv + (double)p;
-          pend = pend + (double)p;
-          left = left + w;
         }
-      }
-      if (isD && dme == id) {
-        owed = owed + (double)(o - 1) * dec_tok_ns;
-        q += 1;
-        kv = kv + ((double)p + (double)o);
-        pend = pend + (double)oh;
-      }
+        if (isD && sl == wd && m == md) {
+          x.owed = x.owed + (double)(o - 1) * dec_tok_ns;
+          x.q += 1;
+          x.kv = x.kv + ((double)p + (double)o);
+          x.pend = x.pend + (double)oh;
+        }
+      });
     }
     // a replica whose ring overflowed stops (its outputs are not valid)
     dead = seg_or<S>(full ? 1u : 0u, lane) != 0;
@@ -933,15 +1032,17 @@ hipError_t launch_bat(const SimClass& c, const SimArgs& a, const BatScratch& b, 
   const int64_t lanes = a.n_work * (int64_t)c.S;
   const dim3 grid((unsigned)((lanes + bat::kBlock - 1) / bat::kBlock)), block(bat::kBlock);
   // with at least two waves per SIMD to place, occupancy pays more than
-  // registers do
+  // registers do; two instances per lane fit two waves per SIMD without
+  // spilling, three spill (measured on 16,384 replicas of 8 + 64 instances:
+  // two waves 27.5 ms, three 51.3 ms)
   const bool many = lanes >= 2 * 64 * 1024;
-#define RT_BSEG_CASE(S_)                                                              \
-  if (c.MP == 1 && c.S == S_) {                                                       \
-    if (many)                                                                         \
-      hipLaunchKernelGGL((bat::bseg_kernel<S_, 3>), grid, block, 0, stream, a, b);    \
-    else                                                                              \
-      hipLaunchKernelGGL((bat::bseg_kernel<S_, 1>), grid, block, 0, stream, a, b);    \
-    return hipGetLastError();                                                         \
+#define RT_BSEG_CASE(S_, M_)                                                              \
+  if (c.MP == M_ && c.S == S_) {                                                          \
+    if (many)                                                                             \
+      hipLaunchKernelGGL((bat::bseg_kernel<S_, M_ == 1 ? 3 : 2, M_>), grid, block, 0, stream, a, b);  \
+    else                                                                                  \
+      hipLaunchKernelGGL((bat::bseg_kernel<S_, 1, M_>), grid, block, 0, stream, a, b);    \
+    return hipGetLastError();                                                             \
   }
   RT_BSEG_FOR_EACH(RT_BSEG_CASE)
 #undef RT_BSEG_CASE

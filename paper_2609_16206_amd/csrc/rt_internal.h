@@ -113,11 +113,12 @@ struct BatScratch {
 // carving of one allocation into it.
 size_t bat_scratch_bytes(int64_t S, int32_t NI, int32_t C);
 BatScratch bat_scratch_carve(char* base, int64_t S, int32_t NI, int32_t C);
-// Batched classes: one replica per aligned segment of S lanes, one instance
-// per lane (P + D <= S; MP = MD = 1), then the general one, one replica per
-// lane (S = 1, MP = MD = 0).  bat_lanes: the lanes a launch spans, each the
-// owner of one state slot and one ring pair in the class's scratch.
-#define RT_BSEG_FOR_EACH(X) X(4) X(8) X(16) X(32) X(64)
+// Batched classes {S, M}: one replica per aligned segment of S lanes, M
+// instances per lane (ceil(P / M) + ceil(D / M) <= S; MP = MD = M), then the
+// general one, one replica per lane (S = 1, MP = MD = 0).  bat_lanes: the
+// lanes a launch spans, each the owner of NI state slots and NI ring pairs in
+// the class's scratch (NI = M for a segment class).
+#define RT_BSEG_FOR_EACH(X) X(4, 1) X(8, 1) X(16, 1) X(32, 1) X(64, 1) X(64, 2)
 hipError_t launch_bat(const SimClass& c, const SimArgs& a, const BatScratch& b, hipStream_t stream);
 int64_t bat_lanes(const SimClass& c, int64_t n_work);
 

@@ -25,9 +25,9 @@ constexpr int kNumWide = (int)(sizeof(kWideShapes) / sizeof(kWideShapes[0]));
 constexpr int kModes[] = {kModeTrue, kModeProxy, kModeBase, kModeTrueSampled, kModeProxySampled};
 constexpr int kNumModes = (int)(sizeof(kModes) / sizeof(kModes[0]));
 
-// Batched-service shapes {S, M}: the segment ones (M = 1), then the general
-// one-replica-per-lane class {1, 0}.
-#define RT_BSEG_SHAPE(S_) {S_, 1},
+// Batched-service shapes {S, M}: the segment ones (one instance per lane
+// first, then two), then the general one-replica-per-lane class {1, 0}.
+#define RT_BSEG_SHAPE(S_, M_) {S_, M_},
 const SegShape kBatShapes[] = {RT_BSEG_FOR_EACH(RT_BSEG_SHAPE){1, 0}};
 #undef RT_BSEG_SHAPE
 constexpr int kNumBat = (int)(sizeof(kBatShapes) / sizeof(kBatShapes[0]));

@@ -72,9 +72,10 @@ def test_mixed_shapes_betas_and_serial_points():
     """Batched points of several pool shapes and betas (0: infinite server;
     1: pure processor sharing) next to serial points in one call, so both
     kernel kinds run side by side; ragged and empty replicas."""
-    # segment widths 4, 8, 16, 32 and 64 (P + D = 64 exactly), and beyond 64
-    # instances the one-replica-per-lane kernel
-    shapes = [(1, 1), (2, 6), (3, 9), (5, 16), (8, 8), (33, 64), (2, 2), (4, 12), (32, 32), (20, 44)]
+    # segment widths 4, 8, 16, 32 and 64 (P + D = 64 exactly), two instances
+    # per lane up to 128 instances, and beyond that the one-replica-per-lane
+    # kernel
+    shapes = [(1, 1), (2, 6), (3, 9), (5, 16), (8, 8), (33, 64), (2, 2), (4, 12), (32, 32), (20, 44), (40, 100)]
     betas = [(0.0, 0.0), (W.BATCH_BETA, W.BATCH_BETA), (1.0, 0.25), (0.5, 1.0)]
     pts = []
     for k, (P, D) in enumerate(shapes):
@@ -184,8 +185,8 @@ def test_wide_bench_workload_sampled():
 
 def test_wide_pool_bench_workload_sampled():
     """The batched bench workload whose pool (8 prefill + 64 decode) is too
-    wide for a segment, in the launch bench.py times (the one-replica-per-lane
-    kernel): properties on every request, goodput recount on every replica,
+    wide for one instance per lane, in the launch bench.py times (two
+    instances per lane of a 64-lane segment): properties on every request, goodput recount on every replica,
     follow-mode parity on a spread sample of replicas."""
     wl = W.batched_wide_pool()
     tr = W.make_trace(wl)
@@ -198,23 +199,45 @@ def test_wide_pool_bench_workload_sampled():
     log(f"batched wide pool {wl.n_replicas}x{wl.requests}: {rep}; mean goodput {g.mean():.4f}")
 
 
-def test_coarse_grid_ties_many_small_replicas():
-    """Hundreds of small replicas on a coarse time grid with tiny integer
-    physics and transfers of zero: simultaneous arrivals, equal finish times
-    within a batch, completions and KV landings at the same instant, zero
-    decode work (o = 1).  Every replica is checked against the oracle."""
-    rng = np.random.default_rng(91)
+def test_two_instances_per_lane_pools():
+    """Pools of 65 to 128 instances, two per lane of a 64-lane segment: odd
+    and even pool sizes on both sides (P = 65 with D = 1 as well as P = 2 with
+    D = 126), every policy, several betas, ragged and empty replicas, each
+    followed against the oracle."""
+    shapes = [(33, 64), (5, 99), (64, 64), (65, 1), (2, 126), (9, 60), (17, 111)]
+    betas = [(W.BATCH_BETA, W.BATCH_BETA), (0.0, 0.0), (1.0, 0.25), (0.5, 1.0)]
+    pts = []
+    for k, (P, D) in enumerate(shapes):
+        pol, mode = POLICIES[k % len(POLICIES)]
+        bp, bd = betas[k % len(betas)]
+        base = W.make_point(P, D, n_classes=3, policy=pol, backlog_mode=mode, kv_cap=50_000, len_threshold=200)
+        pts.append(_batched(base, bp, bd, batch_cap=4096))
+    lengths = [900, 3, 1, 257, 0, 64, 1200, 129, 40, 700, 2, 300, 65, 0]
+    tr = _ragged(pts, lengths, seed=23, rate_scale=2.0)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    check_properties(pts, tr, gpu)
+    assert np.array_equal(goodput_recount(pts, tr, gpu), met)
+    rep = follow_replicas(pts, tr, gpu, range(len(lengths)), gpu_goodput=g, gpu_met=met)
+    log(f"batched two per lane: {rep}")
+
+
+def _coarse_grid(seed, pool_range, n_rep, max_len):
+    """Replicas on a coarse time grid with tiny integer physics and transfers
+    of zero: simultaneous arrivals, equal finish times within a batch,
+    completions and KV landings at the same instant, zero decode work
+    (o = 1)."""
+    rng = np.random.default_rng(seed)
     pts = []
     for k in range(12):
         pol, mode = POLICIES[k % len(POLICIES)]
-        pt = _batched(W.make_point(int(rng.integers(1, 4)), int(rng.integers(1, 4)), n_classes=2, policy=pol,
-                                   backlog_mode=mode, len_threshold=3),
+        pt = _batched(W.make_point(int(rng.integers(*pool_range)), int(rng.integers(*pool_range)), n_classes=2,
+                                   policy=pol, backlog_mode=mode, len_threshold=3),
                       float(rng.choice([0.0, 0.125, 0.5, 1.0])), float(rng.choice([0.0, 0.25, 1.0])))
         pt.update(pre_base_ns=int(rng.choice([0, 4])), pre_tok_ns=int(rng.choice([1, 2])),
                   dec_tok_ns=int(rng.choice([1, 3])), xfer_tok_ns=int(rng.choice([0, 1])))
         pts.append(pt)
-    n_rep = 480
-    lengths = rng.integers(1, 41, n_rep)
+    lengths = rng.integers(1, max_len + 1, n_rep)
     parts = {k: [] for k in ("arrival_ns", "prompt_len", "out_len", "pred_out_len", "slo_class")}
     for n in lengths:
         parts["arrival_ns"].append(np.sort(rng.integers(0, 12, n)).astype(np.int64) * 4)
@@ -225,8 +248,26 @@ def test_coarse_grid_ties_many_small_replicas():
     tr = {k: np.concatenate(v) for k, v in parts.items()}
     tr["offsets"] = np.concatenate(([0], np.cumsum(lengths))).astype(np.int64)
     tr["param_point"] = (np.arange(n_rep) % len(pts)).astype(np.int32)
-    W.add_sample_words(tr, 91)
+    W.add_sample_words(tr, seed)
+    return pts, tr
+
+
+def test_coarse_grid_ties_many_small_replicas():
+    """Hundreds of small replicas (pools of 1 to 3 per side) on the coarse
+    grid; every replica is checked against the oracle."""
+    pts, tr = _coarse_grid(91, (1, 4), 480, 40)
     gpu, g, met, flags = run_sim(pts, tr)
     assert flags == 0
-    rep = follow_replicas(pts, tr, gpu, range(n_rep), gpu_goodput=g, gpu_met=met)
+    rep = follow_replicas(pts, tr, gpu, range(480), gpu_goodput=g, gpu_met=met)
     log(f"batched coarse grid: {rep}")
+
+
+def test_coarse_grid_ties_wide_pools():
+    """The coarse grid on pools of 33 to 64 per side (66 to 128 instances, two
+    per lane): ties between the two instances of one lane and between lanes;
+    every replica is checked."""
+    pts, tr = _coarse_grid(92, (33, 65), 96, 200)
+    gpu, g, met, flags = run_sim(pts, tr)
+    assert flags == 0
+    rep = follow_replicas(pts, tr, gpu, range(96), gpu_goodput=g, gpu_met=met)
+    log(f"batched coarse grid, wide pools: {rep}")
