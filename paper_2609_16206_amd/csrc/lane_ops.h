@@ -239,6 +239,28 @@ __device__ __forceinline__ void seg_bcast2_f64(double& x, bool ox, double& y, bo
   y = __hiloint2double((int)d, (int)c);
 }
 
+// Values of two lanes of each segment, read by every lane of it: x from
+// segment lane lx and y from segment lane ly (each in [0, S)), one
+// ds_bpermute per 32-bit half (no memory access: the lanes exchange through
+// the LDS crossbar).
+template <int S>
+__device__ __forceinline__ void seg_pick2_f64(double& x, int32_t lx, double& y, int32_t ly, int lane) {
+  const int base = lane & ~(S - 1);
+  const int ax = (base + lx) << 2, ay = (base + ly) << 2;
+  const int xl = __builtin_amdgcn_ds_bpermute(ax, __double2loint(x));
+  const int xh = __builtin_amdgcn_ds_bpermute(ax, __double2hiint(x));
+  const int yl = __builtin_amdgcn_ds_bpermute(ay, __double2loint(y));
+  const int yh = __builtin_amdgcn_ds_bpermute(ay, __double2hiint(y));
+  x = __hiloint2double(xh, xl);
+  y = __hiloint2double(yh, yl);
+}
+
+// A 32-bit value of segment lane lv, read by every lane of the segment.
+template <int S>
+__device__ __forceinline__ int32_t seg_pick(int32_t v, int32_t lv, int lane) {
+  return __builtin_amdgcn_ds_bpermute(((lane & ~(S - 1)) + lv) << 2, v);
+}
+
 // Lowest lane (relative to the segment, or to the wave for S >= 64) of each
 // segment where `pred` holds; -1 where it holds nowhere.
 template <int S>

@@ -132,10 +132,16 @@ __device__ __forceinline__ void merge_pending(Slot& s) {
 // Materializes the merged positions here, ahead of every later memory
 // instruction (an empty volatile asm that reads the registers and clobbers
 // memory), so that the wait for their load is not pushed past the stores.
+// Without a priced ledger the positions' ledger tokens are never read, and
+// are not pinned (so their selects are dropped).
+template <bool kTok>
 __device__ __forceinline__ void pin_window(const Slot& s) {
-  asm volatile("" ::"v"(s.n.t), "v"(s.n.idx), "v"(s.n.fp), "v"(s.n.pt), "v"(s.n2.t), "v"(s.n2.idx), "v"(s.n2.fp),
-               "v"(s.n2.pt)
-               : "memory");
+  if constexpr (kTok)
+    asm volatile("" ::"v"(s.n.t), "v"(s.n.idx), "v"(s.n.fp), "v"(s.n.pt), "v"(s.n2.t), "v"(s.n2.idx), "v"(s.n2.fp),
+                 "v"(s.n2.pt)
+                 : "memory");
+  else
+    asm volatile("" ::"v"(s.n.t), "v"(s.n.idx), "v"(s.n.fp), "v"(s.n2.t), "v"(s.n2.idx), "v"(s.n2.fp) : "memory");
 }
 
 // Byte offset of request g's record in its pool's plane (a shift that folds
@@ -468,19 +474,28 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     seg_min2<S>(kp, kd, lane);
     const int32_t wp = seg_first<S>(kp0 == kp, lane);  // winning lanes
     const int32_t wd = seg_first<S>(kd0 == kd, lane);
-    int32_t mp = 0, md = 0;  // winning slots
-    if constexpr (M > 1) {
-      mp = (int32_t)seg_or<S>(sl == wp ? (uint32_t)bm : 0u, lane);
-      md = (int32_t)seg_or<S>(sl == wd ? (uint32_t)bm : 0u, lane);
+    // the winning slots and the winners' busy-until, read by every lane of
+    // the segment (so that every lane forms both ends): from 8 lanes up
+    // through lane permutes, below that through DPP reductions
+    int32_t mp = 0, md = 0;
+    double busy_p = bbusy, busy_d = bbusy;
+    if constexpr (S >= 8) {
+      seg_pick2_f64<S>(busy_p, wp, busy_d, wd, lane);
+      if constexpr (M > 1) {
+        mp = seg_pick<S>(bm, wp, lane);
+        md = seg_pick<S>(bm, wd, lane);
+      }
+    } else {
+      if constexpr (M > 1) {
+        mp = (int32_t)seg_or<S>(sl == wp ? (uint32_t)bm : 0u, lane);
+        md = (int32_t)seg_or<S>(sl == wd ? (uint32_t)bm : 0u, lane);
+      }
+      seg_bcast2_f64<S>(busy_p, sl == wp, busy_d, sl == wd, lane);
     }
     const int32_t ip = wp * M + mp;
     const int32_t id = (wd - LP) * M + md;
 
     // 3. serve: prefill, KV transfer, decode (exact integers in doubles)
-    // (the winners' busy-until, broadcast over the segment, so that every
-    // lane forms both ends)
-    double busy_p = bbusy, busy_d = bbusy;
-    seg_bcast2_f64<S>(busy_p, sl == wp, busy_d, sl == wd, lane);
     const double s_pre = __builtin_fma((double)p, pre_tok_ns, pre_base_ns);
     const double pf_end = __builtin_fmax(now, busy_p) + s_pre;
     const double kv_at = pf_end + (double)p * xfer_tok_ns;
@@ -545,7 +560,7 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
 #pragma unroll
     for (int m = 0; m < M; ++m) {
       merge_pending(s[m]);
-      pin_window(s[m]);
+      pin_window<kTok>(s[m]);
     }
     if constexpr (kSamp)
       asm volatile("" : "+v"(nx.arr), "+v"(nx.p), "+v"(nx.o), "+v"(nx.oh), "+v"(nx.c), "+v"(nx.u), "+v"(nx.v));
