@@ -81,7 +81,7 @@ def _source_hash(files):
 SIM_SOURCES = ["paper_2609_16206_amd/csrc/" + f for f in (
     "seg_kernel.h", "wseg_kernel.h", "seg_true.hip", "seg_proxy.hip", "seg_base.hip", "seg_true_s.hip", "seg_proxy_s.hip", "seg_classes.hip",
     "lane_ops.h", "rt_internal.h", "api.hip")]
-BAT_SOURCES = ["paper_2609_16206_amd/csrc/" + f for f in ("bat_kernel.hip", "lane_ops.h", "rt_internal.h", "api.hip")]
+BAT_SOURCES = ["paper_2609_16206_amd/csrc/" + f for f in ("bat_kernel.hip", "lane_ops.h", "rt_internal.h", "api.hip", "seg_classes.hip")]
 SCORE_SOURCES = ["paper_2609_16206_amd/csrc/score_kernel.hip", "paper_2609_16206_amd/csrc/rt_internal.h"]
 
 
