@@ -66,7 +66,7 @@ typedef enum {
   RT_POLICY_LEARNED = 0,      /* the marginal-cost scorer (Section III-A)              */
   RT_POLICY_ROUND_ROBIN = 1,  /* request r goes to instance r mod N (Section IV-C)     */
   RT_POLICY_LEAST_LOADED = 2, /* fewest in-flight requests, lowest index on ties       */
-  RT_POLICY_LEARNED_SAMPLED = 3, /* the scorer over two random candidates per pool: the
+  RT_POLICY_LEARNED_SAMPLED = 3, /* the scorer over two randomly drawn candidates per pool: the
                                    sampled variant that Section V-E and Section VI give
                                    as the mitigation for scarce pools (candidates: see
                                    rt_sim_run_replicas)                                */
@@ -88,7 +88,7 @@ typedef enum { RT_POOL_PREFILL = 0, RT_POOL_DECODE = 1 } rt_pool;
 typedef enum {
   RT_SERVICE_SERIAL = 0,  /* one request at a time per instance, in admission order
                              (the serial-service model of Section III-D / VI)        */
-  RT_SERVICE_BATCHED = 1  /* continuous batching in both stages (the model Section VI
+  RT_SERVICE_BATCHED = 1  /* continuous batching at the prefill and the decode stage alike (the model Section VI
                              adds): every admitted request is served at once, each at
                              1 / (1 + beta (b - 1)) of its stand-alone speed while b
                              requests share the instance (see rt_sim_run_replicas)  */

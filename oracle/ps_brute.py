@@ -2,8 +2,8 @@
 (test infrastructure).
 
 A second, independent implementation of the model the C oracle's
-orc_sim_replica_batched follows (Section VI: continuous batching in both
-stages, each request slowed by 1 + beta (b - 1) while b requests share an
+orc_sim_replica_batched follows (Section VI: both stages batched
+continuously, each request slowed by 1 + beta (b - 1) while b requests share an
 instance), written the other way round: instead of a virtual clock per
 instance it keeps every request's remaining stand-alone work and, between
 consecutive events, takes dt / (1 + beta (b - 1)) off each request of every

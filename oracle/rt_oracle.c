@@ -440,7 +440,7 @@ int64_t orc_goodput(const orc_point* pt, int64_t n, const int32_t* out_len,
 
 
 /* ------------------------------------------------------------------------ */
-/* Continuous batching in both stages (Section VI): processor sharing with a */
+/* Continuous batching at the prefill and the decode stage alike (Section VI): processor sharing with a */
 /* batch-dependent speed.  See rt_oracle.h for the model.                   */
 /* ------------------------------------------------------------------------ */
 
@@ -612,7 +612,7 @@ static int b_run_to(bsim* b, double T) {
 }
 
 /* Features of one pool.  Clock backlog (backlog(d) of Section III-A, the
- * work already committed to the instance, under batching): the stand-alone
+ * work the instance has taken on and not yet done, under batching): the stand-alone
  * work (ns) the instance still owes, summed over the batch in member order,
  * each member's max(f - v, 0) (clamped as in b_next), plus, on a decode
  * instance, the whole work of the requests routed there that have not

@@ -18,8 +18,8 @@
  *                       optionally in "follow" mode, where it adopts
  *                       externally supplied placements and accounts every
  *                       divergence from its own choice;
- *   - orc_sim_replica_batched: the same replica under continuous batching
- *                       in both stages (processor sharing with a
+ *   - orc_sim_replica_batched: the same replica with both stages
+ *                       batched continuously (processor sharing with a
  *                       batch-dependent slowdown);
  *   - orc_goodput:      fraction of a replica's requests meeting both the
  *                       TTFT and the TPOT target of their class.
@@ -41,7 +41,7 @@ extern "C" {
 
 #define ORC_MAX_CLASSES 8
 
-/* ORC_LEARNED_SAMPLED: the learned score over two random candidates per pool
+/* ORC_LEARNED_SAMPLED: the learned score over two randomly drawn candidates per pool
  * (the sampled variant Section V-E and Section VI name as the mitigation for
  * scarce pools).  The random words are inputs (see orc_candidates). */
 /* ORC_LENGTH_THRESHOLD: the predicted-length threshold baseline (Section
@@ -135,7 +135,7 @@ int orc_sim_replica(const orc_point* pt, int64_t n, const int64_t* arrival_ns,
                     int32_t* i_pre, int32_t* i_dec, int64_t* ttft_ns, int64_t* span_ns,
                     orc_stats* st);
 
-/* The same replica under continuous batching in both stages (the service
+/* The same replica under continuous batching at the prefill and the decode stage alike (the service
  * model Section VI adds to the serial one): every instance serves all its
  * admitted requests at once, each at 1 / (1 + beta * (b - 1)) of its
  * stand-alone speed while b requests share the instance (beta_pre for

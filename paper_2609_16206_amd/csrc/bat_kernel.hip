@@ -1,5 +1,5 @@
 // Replica-batched simulation of the learned prefill/decode router under
-// continuous batching in both stages, on gfx950.
+// continuous batching at the prefill and the decode stage alike, on gfx950.
 //
 // Model (the service model Section VI adds to the serial one; routing is
 // Algorithm 1 with the Section III-A cost equation, unchanged): every

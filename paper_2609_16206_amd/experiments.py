@@ -16,7 +16,7 @@ the router:
     per prompt and per output token fitted to latency curves by least
     squares;
   * service_cells / the `service` study: the serial-service model next to
-    continuous batching in both stages (Section VI's correction), per
+    continuous batching at the prefill and the decode stage alike (Section VI's correction), per
     policy at one arrival rate, with goodput and tail TTFT, and the
     saturation scale under each model.
 
@@ -211,8 +211,8 @@ BATCH_ROOM = 4096
 
 def service_cells(P: int, D: int, traffic: W.Traffic, policies=("learned", "round_robin", "least_loaded"),
                   beta: float = W.BATCH_BETA, **kw) -> List[Cell]:
-    """Each policy under the serial-service model and under continuous
-    batching in both stages (Section VI), at the same arrival rate."""
+    """Each policy under the serial-service model and with both stages
+    batched continuously (Section VI), at the same arrival rate."""
     cells = []
     for pol in policies:
         for sv in ("serial", "batched"):

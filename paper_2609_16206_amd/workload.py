@@ -147,7 +147,7 @@ def make_point(
     true service model (int64 ns).  ``tau_*_scale`` multiplies the router's
     per-token prices relative to the physics (1.0 = calibrated, Section III-B).
     ``service`` is "serial" (one request at a time per instance) or "batched"
-    (continuous batching in both stages: each of b requests sharing an
+    (continuous batching at the prefill and the decode stage alike: each of b requests sharing an
     instance runs at 1 / (1 + beta (b - 1)) of its stand-alone speed);
     both betas default to BATCH_BETA, the measured decode curve of Section VI.
     """
@@ -549,7 +549,7 @@ def large_pool_wl(n_replicas: int = 256, requests: int = 1_000_000, seed: int = 
 
 def batched_wide_pool(n_replicas: int = 16384, requests: int = 1000, seed: int = 5, n_prefill: int = 8,
                       n_decode: int = 64, load: float = 0.8) -> Workload:
-    """Continuous batching in both stages on a pool too wide for one segment
+    """Continuous batching at the prefill and the decode stage alike on a pool too wide for one segment
     of lanes (8 prefill + 64 decode = 72 instances): mixed bursty traffic at
     ``load`` x the serial-service capacity."""
     pt = make_point(n_prefill, n_decode, n_classes=3, service="batched")

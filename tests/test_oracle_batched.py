@@ -1,5 +1,5 @@
 """Pins of the oracle's continuous-batching service model (Section VI: the
-paper's correction to the serial model, continuous batching in both stages,
+paper's correction to the serial model, continuous batching at the prefill and the decode stage alike,
 a batch of b slowing each member by 1 + beta (b - 1)).  CPU only.
 
 What fixes it, beyond the oracle's own code:

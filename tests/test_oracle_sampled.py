@@ -1,5 +1,5 @@
-"""Pins of the oracle's sampled policy: the learned score over two random
-candidates per pool (the mitigation Section V-E and Section VI name for
+"""Pins of the oracle's sampled policy: the learned score over two randomly
+drawn candidates per pool (the mitigation Section V-E and Section VI name for
 scarce pools).  CPU only.
 
 What fixes it, beyond the oracle's own code:
