@@ -222,6 +222,25 @@ def test_two_instances_per_lane_pools():
     log(f"batched two per lane: {rep}")
 
 
+def test_two_instances_per_lane_ring_capacity():
+    """The ring-capacity flag and the stop of an overflowing replica with two
+    instances per lane (a 9 + 91 pool): a batch_cap of 2 under eight times
+    the load sets flag bit 3; with room, every replica is exact."""
+    base = W.make_point(9, 91, n_classes=3)
+    small = _batched(base, batch_cap=2)
+    roomy = _batched(base, batch_cap=4096)
+    lengths = [400, 1, 250, 0, 333]
+    tr = _ragged([small], lengths, seed=29, rate_scale=8.0)
+    gpu, _, _, flags = run_sim([small], tr)
+    assert flags & 8
+    tr = _ragged([roomy], lengths, seed=29, rate_scale=8.0)
+    gpu, g, met, flags = run_sim([roomy], tr)
+    assert flags == 0
+    check_properties([roomy], tr, gpu)
+    rep = follow_replicas([roomy], tr, gpu, range(len(lengths)), gpu_goodput=g, gpu_met=met)
+    log(f"batched two per lane, ring capacity: {rep}")
+
+
 def _coarse_grid(seed, pool_range, n_rep, max_len):
     """Replicas on a coarse time grid with tiny integer physics and transfers
     of zero: simultaneous arrivals, equal finish times within a batch,
