@@ -323,7 +323,7 @@ def main():
                          "hardware byte counters when the run is profiled)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps(dict(error="this build measures one GPU: replicas are independent and would shard "
+        print(json.dumps(dict(error="bench.py measures one GPU: replicas are independent and would shard "
                                     "across GPUs with no exchange, but only --gpus 1 is run")), flush=True)
         sys.exit(2)
     if args.calibrate_copy > 0:

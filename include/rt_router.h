@@ -58,7 +58,7 @@ typedef enum {
   RT_ENOMEM = -2,       /* device or host allocation failed                              */
   RT_EDEVICE = -3,      /* a HIP runtime call failed                                     */
   RT_ERANGE = -4,       /* a size beyond a documented limit                              */
-  RT_EUNSUPPORTED = -5, /* a pool shape this build has no kernel for                     */
+  RT_EUNSUPPORTED = -5, /* a pool shape the library has no kernel for                   */
   RT_EDATA = -6         /* the device flag word reports rejected requests                */
 } rt_status;
 

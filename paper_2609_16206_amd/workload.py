@@ -55,8 +55,8 @@ def f32(x: float) -> float:
 # --------------------------------------------------------------------------
 # The simulator set: decode 0.0018 s/token, prefill base 0.005 s, 2048 KV
 # bytes/token.  The paper gives neither a prefill per-token time nor a link
-# bandwidth; the values below (1e-5 s/token, 25 GB/s) are this build's
-# readings and are flagged as such in the design notes.
+# bandwidth; the values below (1e-5 s/token, 25 GB/s) are readings of this
+# library, not the paper's.
 LINK_BYTES_PER_S = 25e9
 
 SIM_PHYSICS = dict(
@@ -78,7 +78,8 @@ A40_PHYSICS = dict(
 # Continuous batching (Section VI): the measured decode curve is nearly flat,
 # a batch of eight costing each request 2.9 % more per token, i.e. a factor
 # 1 + beta (b - 1) with beta = 0.029 / 7 per extra batch member.  The paper
-# gives no prefill curve; the same beta for prefill is this build's reading.
+# gives no prefill curve; the same beta for prefill is a reading of this
+# library.
 BATCH_BETA = 0.029 / 7
 
 
@@ -110,7 +111,7 @@ def slo_targets(dec_tok_ns: int, n_classes: int):
 def sigma_table(n_classes: int) -> List[float]:
     """SLO amplifier sigma(s) (Section III-A): larger for tighter classes.
 
-    The paper gives no values; this build reads sigma_c = 1 + 3^-c, rounded to
+    The paper gives no values; this library reads sigma_c = 1 + 3^-c, rounded to
     float32 once (2, 1.3333334, 1.1111112, 1.0370370, ...).
     """
     out = [1.0] * MAX_CLASSES
