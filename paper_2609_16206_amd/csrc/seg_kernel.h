@@ -258,10 +258,26 @@ __device__ __forceinline__ void release_slot(Slot& x, double now_eff, const char
   load_refill<kTok>(x, recr, R, dmy);
 }
 
+// The releases of every slot.  With one slot per lane they run on every
+// step, branch-free (a launch of such classes has about one wave per SIMD,
+// and a branch costs more than the work it skips).  With two or more, a slot
+// whose head has finished on no lane of the wave is skipped, and the refill
+// load is issued only where some lane needs one (those classes run several
+// waves per SIMD and are bound by instruction issue: sweep 60.3 -> 55.3 ms
+// with the matching merge below).
 template <int M, bool kTok, bool kKv>
 __device__ __forceinline__ void release_fast(Slot (&s)[M], double now_eff, const char* recr, int32_t R, int64_t dmy) {
-#pragma unroll
-  for (int m = 0; m < M; ++m) release_slot<kTok, kKv>(s[m], now_eff, recr, R, dmy);
+  static_for<M>([&](auto mc) __attribute__((always_inline)) {
+    constexpr int m = decltype(mc)::value;
+    if constexpr (M >= 2) {
+      if (__any(s[m].h.t <= now_eff)) {
+        release_pop<kTok, kKv>(s[m], now_eff);
+        if (__any(s[m].lq != 0)) load_refill<kTok>(s[m], recr, R, dmy);
+      }
+    } else {
+      release_slot<kTok, kKv>(s[m], now_eff, recr, R, dmy);
+    }
+  });
 }
 
 template <int M>
@@ -556,12 +572,20 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     // 5. the successors loaded during request t's releases (the step's one
     // wait: those loads and the features of request t+1 were issued a step
     // ago), kept apart from the surrounding code by the scheduling barriers
+    // (with two or more slots per lane, only slots where some lane loaded)
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int m = 0; m < M; ++m) {
-      merge_pending(s[m]);
-      pin_window<kTok>(s[m]);
-    }
+    static_for<M>([&](auto mc) __attribute__((always_inline)) {
+      constexpr int m = decltype(mc)::value;
+      if constexpr (M >= 2) {
+        if (__any(s[m].lq != 0)) {
+          merge_pending(s[m]);
+          pin_window<kTok>(s[m]);
+        }
+      } else {
+        merge_pending(s[m]);
+        pin_window<kTok>(s[m]);
+      }
+    });
     if constexpr (kSamp)
       asm volatile("" : "+v"(nx.arr), "+v"(nx.p), "+v"(nx.o), "+v"(nx.oh), "+v"(nx.c), "+v"(nx.u), "+v"(nx.v));
     else
