@@ -109,7 +109,7 @@ struct Lane {
   // A prefill completion of request r at time tc: the instance lets go of
   // its tokens, TTFT is recorded, the prefill end is kept in the span slot
   // until decode ends, and the KV leaves for the decode instance.
-  __device__ void prefill_done(int32_t j, int32_t r, double tc, int32_t& q, double& kv, double& pend) {
+  __device__ void prefill_done(int32_t r, double tc, int32_t& q, double& kv, double& pend) {
     const int64_t g = lo + r;
     const int32_t p = a.plen[g];
     q -= 1;
@@ -157,7 +157,7 @@ struct Lane {
       tl = tc;
       tmax = fmax(tmax, tc);
       for (;;) {
-        prefill_done(j, e.r, tc, q, kv, pend);
+        prefill_done(e.r, tc, q, kv, pend);
         ++head;
         --nact;
         if (nact == 0) break;
@@ -927,13 +927,13 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
     }
     uint32_t kp = isP ? bkey : 0xffffffffu, kd = isD ? bkey : 0xffffffffu;
     const uint32_t kp0 = kp, kd0 = kd;
-    seg_min2<S>(kp, kd, lane);
+    seg_min2<S>(kp, kd);
     const int32_t wp = seg_first<S>(isP && kp0 == kp, lane);  // winning lanes
     const int32_t wd = seg_first<S>(isD && kd0 == kd, lane);
     int32_t mp = 0, md = 0;  // winning slots
     if constexpr (M > 1) {
-      mp = (int32_t)seg_or<S>(sl == wp ? (uint32_t)bm : 0u, lane);
-      md = (int32_t)seg_or<S>(sl == wd ? (uint32_t)bm : 0u, lane);
+      mp = (int32_t)seg_or<S>(sl == wp ? (uint32_t)bm : 0u);
+      md = (int32_t)seg_or<S>(sl == wd ? (uint32_t)bm : 0u);
     }
     const int32_t ip = wp * M + mp;
     const int32_t id = (wd - LP) * M + md;
@@ -974,7 +974,7 @@ __global__ __launch_bounds__(kBlock, kMinBlocks) void bseg_kernel(SimArgs a, Bat
       });
     }
     // a replica whose ring overflowed stops (its outputs are not valid)
-    dead = seg_or<S>(full ? 1u : 0u, lane) != 0;
+    dead = seg_or<S>(full ? 1u : 0u) != 0;
   }
   run_to(kInf);
   const uint32_t flag = (tmax >= kTimeLimit ? kFlagTimeRange : 0u) | (rej ? kFlagRejected : 0u) |

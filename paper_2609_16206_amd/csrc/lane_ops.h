@@ -162,19 +162,10 @@ __device__ __forceinline__ uint32_t cross_rows(uint32_t v, Op op) {
   return v;
 }
 
-template <int S>
-__device__ __forceinline__ uint32_t seg_min(uint32_t v, int lane) {
-  if constexpr (S >= 2) v = min(v, dpp<0xB1>(v));
-  if constexpr (S >= 4) v = min(v, dpp<0x4E>(v));
-  if constexpr (S >= 8) v = min(v, dpp<0x141>(v));
-  if constexpr (S >= 16) v = min(v, dpp<0x140>(v));
-  return cross_rows<S>(v, [](uint32_t x, uint32_t y) { return min(x, y); });
-}
-
 // Two independent segment minima, interleaved so that each DPP step of one
 // fills the other's data-hazard wait.
 template <int S>
-__device__ __forceinline__ void seg_min2(uint32_t& v, uint32_t& w, int lane) {
+__device__ __forceinline__ void seg_min2(uint32_t& v, uint32_t& w) {
   if constexpr (S >= 2) { v = min(v, dpp<0xB1>(v)); w = min(w, dpp<0xB1>(w)); }
   if constexpr (S >= 4) { v = min(v, dpp<0x4E>(v)); w = min(w, dpp<0x4E>(w)); }
   if constexpr (S >= 8) { v = min(v, dpp<0x141>(v)); w = min(w, dpp<0x141>(w)); }
@@ -184,7 +175,7 @@ __device__ __forceinline__ void seg_min2(uint32_t& v, uint32_t& w, int lane) {
 }
 
 template <int S>
-__device__ __forceinline__ uint32_t seg_or(uint32_t v, int lane) {
+__device__ __forceinline__ uint32_t seg_or(uint32_t v) {
   if constexpr (S >= 2) v |= dpp<0xB1>(v);
   if constexpr (S >= 4) v |= dpp<0x4E>(v);
   if constexpr (S >= 8) v |= dpp<0x141>(v);
@@ -203,27 +194,10 @@ __device__ __forceinline__ int32_t wave_max_nonneg(int32_t v) {
   return (int32_t)u;
 }
 
-// Broadcast a double from the one lane of each segment where `own` holds
-// (every other lane contributes 0 bits to an OR); the two halves are reduced
-// interleaved.
-template <int S>
-__device__ __forceinline__ double seg_bcast_f64(double v, bool own, int lane) {
-  uint32_t lo = own ? (uint32_t)__double2loint(v) : 0u;
-  uint32_t hi = own ? (uint32_t)__double2hiint(v) : 0u;
-  if constexpr (S >= 2) { lo |= dpp<0xB1>(lo); hi |= dpp<0xB1>(hi); }
-  if constexpr (S >= 4) { lo |= dpp<0x4E>(lo); hi |= dpp<0x4E>(hi); }
-  if constexpr (S >= 8) { lo |= dpp<0x141>(lo); hi |= dpp<0x141>(hi); }
-  if constexpr (S >= 16) { lo |= dpp<0x140>(lo); hi |= dpp<0x140>(hi); }
-  const auto orf = [](uint32_t x, uint32_t y) { return x | y; };
-  lo = cross_rows<S>(lo, orf);
-  hi = cross_rows<S>(hi, orf);
-  return __hiloint2double((int)hi, (int)lo);
-}
-
 // Two broadcasts at once: x from the lane of each segment where `ox` holds and
 // y from the one where `oy` holds, the four halves reduced interleaved.
 template <int S>
-__device__ __forceinline__ void seg_bcast2_f64(double& x, bool ox, double& y, bool oy, int lane) {
+__device__ __forceinline__ void seg_bcast2_f64(double& x, bool ox, double& y, bool oy) {
   uint32_t a = ox ? (uint32_t)__double2loint(x) : 0u, b = ox ? (uint32_t)__double2hiint(x) : 0u;
   uint32_t c = oy ? (uint32_t)__double2loint(y) : 0u, d = oy ? (uint32_t)__double2hiint(y) : 0u;
   if constexpr (S >= 2) { a |= dpp<0xB1>(a); b |= dpp<0xB1>(b); c |= dpp<0xB1>(c); d |= dpp<0xB1>(d); }

@@ -487,7 +487,7 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
     // 2. argmin of each pool over the segment, lowest index on equal keys
     uint32_t kp = isp ? bkey : 0xffffffffu, kd = isp ? 0xffffffffu : bkey;
     const uint32_t kp0 = kp, kd0 = kd;
-    seg_min2<S>(kp, kd, lane);
+    seg_min2<S>(kp, kd);
     const int32_t wp = seg_first<S>(kp0 == kp, lane);  // winning lanes
     const int32_t wd = seg_first<S>(kd0 == kd, lane);
     // the winning slots and the winners' busy-until, read by every lane of
@@ -503,10 +503,10 @@ __global__ void __launch_bounds__(64 * kWaves) seg_kernel(SimArgs a) {
       }
     } else {
       if constexpr (M > 1) {
-        mp = (int32_t)seg_or<S>(sl == wp ? (uint32_t)bm : 0u, lane);
-        md = (int32_t)seg_or<S>(sl == wd ? (uint32_t)bm : 0u, lane);
+        mp = (int32_t)seg_or<S>(sl == wp ? (uint32_t)bm : 0u);
+        md = (int32_t)seg_or<S>(sl == wd ? (uint32_t)bm : 0u);
       }
-      seg_bcast2_f64<S>(busy_p, sl == wp, busy_d, sl == wd, lane);
+      seg_bcast2_f64<S>(busy_p, sl == wp, busy_d, sl == wd);
     }
     const int32_t ip = wp * M + mp;
     const int32_t id = (wd - LP) * M + md;
